@@ -1,0 +1,259 @@
+"""Benchmark of the derived-operator hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of the four measured workloads,
+through the public entry points, inputs already resident in HBM:
+  derived_conv2d            ResNet conv3x3, N=16, C=K=256, 14x14            (GEMM + OffsetAdd)
+  derived_conv_transpose2d  DCGAN convT 4x4 s2, N=16, 512->256, 8x8 -> 16x16 (GEMM + selective add)
+  derived_dilated_conv2d    CSRNet dilated conv3x3 d2, C=K=512, 96x128       (GEMM + dilated OffsetAdd)
+  banded_bmm                Longformer band, B=96, L=4096, d=64, w=256, dil 2 (fused G2BMM/softmax/GBMM)
+
+`value` is the step's algorithmic TFLOP/s (all GEMM-stage and band contractions over
+the step time).  Per workload it also reports the GEMM stage in TFLOP/s and % of the
+bf16 MFMA peak and the eOperator stage in GB/s and % of the HBM peak, each timed with
+HIP events around K back-to-back launches of that stage's kernel on the stream it runs
+on.  `roofline` covers the kernel that takes the largest share of a step.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workloads.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def valid_taps_1d(n_in, n_out, r, stride, pad, dil, transposed):
+    """Number of (output position, tap) pairs that read a real input position."""
+    cnt = 0
+    for o in range(n_out):
+        for t in range(r):
+            if transposed:
+                th = o + pad - t * dil
+                if th >= 0 and th % stride == 0 and th // stride < n_in:
+                    cnt += 1
+            else:
+                i = o * stride - pad + t * dil
+                if 0 <= i < n_in:
+                    cnt += 1
+    return cnt
+
+
+def conv_costs(wl, ho, wo, y_bytes=4, out_bytes=4):
+    m = wl.n * wl.h * wl.w
+    nc = wl.r * wl.s * wl.k
+    flops = 2.0 * m * wl.c * nc
+    taps = wl.n * valid_taps_1d(wl.h, ho, wl.r, wl.stride[0], wl.pad[0], wl.dil[0], wl.transposed) \
+        * valid_taps_1d(wl.w, wo, wl.s, wl.stride[1], wl.pad[1], wl.dil[1], wl.transposed)
+    eop_bytes = taps * wl.k * y_bytes + wl.n * ho * wo * wl.k * out_bytes
+    return flops, eop_bytes
+
+
+def band_flops(wl):
+    return 2 * 2.0 * wl.b * wl.l * (2 * wl.w + 1) * wl.d
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this library has no multi-GPU path "
+              "(batch/head sharding needs no communication; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2208_02025_amd as ol
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # ---------------------------------------------------------------- inputs in HBM
+    conv_ops = []
+    for cfg, entry in ((2, ol.derived_conv2d), (3, ol.derived_conv_transpose2d),
+                       (4, ol.derived_dilated_conv2d)):
+        wl = synth.WORKLOADS[cfg]
+        x, wt = synth.conv_inputs(wl)
+        x, wt = x.to(dev), wt.to(dev)
+        desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), wl.stride, wl.pad, wl.dil,
+                            wl.out_pad, x.dtype, torch.float32)
+        ho, wo = ol.conv_out_hw(desc, wl.transposed)
+        out = torch.empty((wl.n, ho, wo, wl.k), dtype=torch.float32, device=dev)
+        ws = torch.empty(ol.conv_workspace_bytes(desc, wl.transposed), dtype=torch.uint8,
+                         device=dev)
+        kw = dict(stride=wl.stride, padding=wl.pad, out=out, ws=ws)
+        if cfg == 3:
+            kw["output_padding"] = wl.out_pad
+        if cfg == 4:
+            kw["dilation"] = wl.dil
+        flops, eop_bytes = conv_costs(wl, ho, wo)
+        conv_ops.append(dict(cfg=cfg, wl=wl, entry=entry, x=x, wt=wt, kw=kw, desc=desc, ws=ws,
+                             out=out, flops=flops, eop_bytes=eop_bytes,
+                             m=wl.n * wl.h * wl.w, nc=wl.r * wl.s * wl.k))
+    bwl = synth.WORKLOADS[5]
+    q, k, v = (t.to(dev) for t in synth.band_inputs(bwl))
+    o = torch.empty(tuple(q.shape), dtype=torch.float32, device=dev)
+    bflops = band_flops(bwl)
+
+    def band_call():
+        ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale, mask_invalid=bwl.mask_invalid,
+                      out=o)
+
+    def step(evs=None):
+        for i, op in enumerate(conv_ops):
+            if evs is not None:
+                evs[i].record(stream)
+            op["entry"](op["x"], op["wt"], **op["kw"])
+        if evs is not None:
+            evs[3].record(stream)
+        band_call()
+        if evs is not None:
+            evs[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ----------------------------------------------------------------- timed steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    op_ms = [sum(evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)) / args.steps
+             for j in range(4)]
+    total_flops = sum(op["flops"] for op in conv_ops) + bflops
+    value = total_flops / (ms_per_step * 1e-3) / 1e12
+
+    # ------------------------------------------------ per-kernel timing (HIP events)
+    def time_kernel(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps   # ms per launch
+
+    reps = max(args.steps, 10)
+    per_cfg = {}
+    kernels = []   # (name, ms per launch, bound, achieved, peak, unit)
+    for op, ms_op in zip(conv_ops, op_ms):
+        y = op["ws"][:op["m"] * op["nc"] * 4].view(torch.float32).view(op["m"], op["nc"])
+        a = op["x"].view(op["m"], op["wl"].c)
+        b = op["wt"].view(op["nc"], op["wl"].c)
+        g_ms = time_kernel(lambda: ol.gemm_nt(a, b, out=y), reps)
+        e_ms = time_kernel(lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y,
+                                                 out=op["out"]), reps)
+        g_tf = op["flops"] / (g_ms * 1e-3) / 1e12
+        e_gb = op["eop_bytes"] / (e_ms * 1e-3) / 1e9
+        name = op["wl"].name
+        per_cfg[name] = {
+            "op_ms": round(ms_op, 5),
+            "gemm_ms": round(g_ms, 5), "gemm_tflops": round(g_tf, 2),
+            "gemm_pct_mfma_peak": round(100 * g_tf / PEAK_BF16_TFLOPS, 2),
+            "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
+            "eop_pct_hbm_peak": round(100 * e_gb / PEAK_HBM_GBS, 2),
+            "gemm_gflop": round(op["flops"] / 1e9, 4), "eop_mbytes": round(op["eop_bytes"] / 1e6, 3),
+        }
+        kernels.append((f"gemm_nt[{name}]", g_ms, "mfma", g_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
+                        op["flops"]))
+        kernels.append((f"eop_gather[{name}]", e_ms, "hbm", e_gb, PEAK_HBM_GBS, "GB/s",
+                        op["eop_bytes"]))
+    b_ms = time_kernel(band_call, reps)
+    b_tf = bflops / (b_ms * 1e-3) / 1e12
+    per_cfg[bwl.name] = {"op_ms": round(op_ms[3], 5), "fused_ms": round(b_ms, 5),
+                         "band_tflops": round(b_tf, 2),
+                         "band_pct_mfma_peak": round(100 * b_tf / PEAK_BF16_TFLOPS, 2),
+                         "band_gflop": round(bflops / 1e9, 3)}
+    kernels.append((f"band_fused[{bwl.name}]", b_ms, "mfma", b_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
+                    bflops))
+    dom = max(kernels, key=lambda t: t[1])
+    roofline = {"kernel": dom[0], "bound": dom[2], "achieved": round(dom[3], 3),
+                "peak": dom[4], "unit": dom[5], "frac": round(dom[3] / dom[4], 4),
+                "traffic": None, "avg_launch_ms": round(dom[1], 5),
+                "algorithmic_per_launch": dom[6]}
+
+    # ---------------------------------------------------------------- CPU baseline
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(conv_ops, bwl)
+
+    line = {
+        "metric": "GEMM TFLOP/s (% MFMA peak) + eOperator GB/s (% HBM peak), per config, 1 GPU",
+        "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "derived conv3x3 (N16 C256 14x14) + convT4x4s2 (N16 512->256 "
+                               "8x8) + dilated conv3x3 d2 (C512 96x128) + band (B96 L4096 d64 "
+                               "w256 dil2), bf16 in, fp32 accumulate/out",
+                   "parallelism": "single GPU"},
+        "per_config": per_cfg,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(conv_ops, bwl):
+    """The oracle (as it stands) on a bounded sample of one step: all outputs of the
+    two small convolutions, a seeded quarter of the dilated convolution's outputs and a
+    seeded 1/32 of the band rows; value = algorithmic flops of the sample / CPU time."""
+    import numpy as np
+    import oracle
+    import synth
+
+    flops = 0.0
+    secs = 0.0
+    rng = np.random.default_rng(0)
+    for op in conv_ops:
+        wl = op["wl"]
+        x, wt = synth.conv_inputs(wl)
+        ho, wo = op["out"].shape[1:3]
+        n_out = wl.n * ho * wo * wl.k
+        frac = 1.0 if wl.cfg != 4 else 0.25
+        idx = None if frac == 1.0 else np.sort(rng.choice(n_out, int(n_out * frac), replace=False))
+        t0 = time.perf_counter()
+        if wl.transposed:
+            oracle.conv_transpose2d(x, wt, wl.stride, wl.pad, wl.dil, wl.out_pad, idx=idx)
+        else:
+            oracle.conv2d(x, wt, wl.stride, wl.pad, wl.dil, idx=idx)
+        secs += time.perf_counter() - t0
+        flops += op["flops"] * frac
+    q, k, v = synth.band_inputs(bwl)
+    n_rows = bwl.b * bwl.l
+    rows = np.sort(rng.choice(n_rows, n_rows // 32, replace=False))
+    t0 = time.perf_counter()
+    oracle.band(q, k, v, bwl.w, bwl.dilation, bwl.scale, bwl.mask_invalid, rows=rows,
+                want_s=False, want_p=False)
+    secs += time.perf_counter() - t0
+    flops += band_flops(bwl) * len(rows) / n_rows
+    return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle", "seconds": round(secs, 2),
+            "sample": "all outputs of the conv3x3 and convT workloads, 25% of the dilated "
+                      "conv outputs, 1/32 of the band rows (seeded); flops scaled to the sample"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,204 @@
+/*
+ * ollie.h -- C ABI of the MI355X (gfx950) derived-operator library.
+ *
+ * The library executes the tensor-algebra expressions that the derivation method
+ * reaches for three convolution operators and a banded batched matmul:
+ *
+ *   convolution-family operator  =  GEMM stage  +  eOperator stage
+ *     GEMM stage   Y[m][n] = sum_c A'[m][c] * K'[c][n]   (the matched Matmul scope,
+ *                  section 4.3.1; operand layouts of Eq. (3) and Eq. (4))
+ *     eOperator    out[p][k] = sum over taps (r,s) of Y[m(p,r,s)][(r*S+s)*K + k]
+ *                  (OffsetAdd of section 2 for convolutions, the selective add of
+ *                  section 6.3 for the strided transposed convolution)
+ *
+ *   banded_bmm   S = G2BMM(Q, K) on the dilated band (Table 2), P = softmax(S),
+ *                O = P * V on the same band; the dilation is removed by splitting
+ *                rows by residue (section 6.4).
+ *
+ * Every tensor pointer is a HIP device pointer.  Every call only enqueues work on
+ * `stream` (a hipStream_t; NULL means the default stream) and returns at once;
+ * results are ready when the stream reaches that point.  The library allocates
+ * nothing and frees nothing: the caller owns every buffer, including workspaces.
+ * No call synchronises the device.
+ *
+ * Errors: each entry point returns an ollie_status.  All argument checks happen on
+ * the host before any HIP call, so a non-zero status other than OLLIE_EHIP means
+ * nothing was enqueued.  OLLIE_EHIP means a HIP launch failed; earlier launches of
+ * the same call may have been enqueued.  ollie_last_error() gives a message for the
+ * last failure on the calling thread.
+ *
+ * Common buffer rules: tensors are dense and row-major in the layouts stated below;
+ * pointers must be 16-byte aligned (else OLLIE_EALIGN); outputs must not alias
+ * inputs or the workspace.
+ */
+#ifndef OLLIE_H
+#define OLLIE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    OLLIE_OK = 0,
+    OLLIE_EINVAL = 1,       /* bad shape, geometry, flag or null pointer        */
+    OLLIE_EDTYPE = 2,       /* unsupported dtype or dtype combination           */
+    OLLIE_EWORKSPACE = 3,   /* workspace smaller than the *_workspace_bytes size */
+    OLLIE_EALIGN = 4,       /* a pointer or a row is not 16-byte aligned         */
+    OLLIE_EHIP = 5          /* a HIP launch failed                              */
+} ollie_status;
+
+typedef enum {
+    OLLIE_F32 = 0,          /* IEEE binary32                                     */
+    OLLIE_BF16 = 1          /* bfloat16; conversions round to nearest even       */
+} ollie_dtype;
+
+/* flags */
+#define OLLIE_Y_BF16            (1u << 1)  /* conv: hold the GEMM scope Y in bf16 (default fp32) */
+#define OLLIE_BAND_STAGED       (1u << 2)  /* band: three kernels through S and P in the workspace */
+#define OLLIE_BAND_MASK_INVALID (1u << 3)  /* band: keys outside [0,l) are left out of the softmax */
+
+/* Geometry of a convolution-family operator.
+ *   X   [n][h][w][c]   input (NHWC).  As a GEMM operand it is A'[m][c] with
+ *                      m = (n*h + hi)*w + wi, i.e. Eq. (3) with a batch dimension:
+ *                      the identity eOperator of section 5.4, no copy is made.
+ *   Wt  [r][s][k][c]   weight (the paper's K[r,s,f,c] with f = k).  Row-major it is
+ *                      the [R*S*K][C] matrix K'^T of Eq. (4), column n = (r*S+s)*k + k.
+ *                      From a torch conv2d weight [K][C][R][S] use permute(2,3,0,1);
+ *                      from a conv_transpose2d weight [C][K][R][S] use permute(2,3,1,0).
+ *                      This layout change depends on weights only and is done once,
+ *                      ahead of time (compile-time evaluation, section 5.4).
+ *   out [n][ho][wo][k] output (NHWC).
+ *   stride, pad, dil >= 1, >= 0, >= 1 per axis; out_pad only for the transposed
+ *   operator (0 <= out_pad < max(stride, dil)), 0 otherwise.
+ *   in_dtype: dtype of X and Wt (F32 or BF16); accumulation is always fp32.
+ *   out_dtype: dtype of out (F32 or BF16). */
+typedef struct {
+    int64_t n, c, h, w;
+    int64_t k, r, s;
+    int32_t stride_h, stride_w;
+    int32_t pad_h, pad_w;
+    int32_t dil_h, dil_w;
+    int32_t out_pad_h, out_pad_w;
+    int32_t in_dtype;      /* ollie_dtype */
+    int32_t out_dtype;     /* ollie_dtype */
+} ollie_conv_desc;
+
+/* Geometry of banded_bmm.
+ *   Q, K, V [b][l][d] bf16, O [b][l][d] (out_dtype F32 or BF16).
+ *   Band entry j in [0, 2w] of row i reads key/value row t = i + (j - w) * dilation;
+ *   rows outside [0, l) read as zero (section 3 padding).
+ *   d must be 64. */
+typedef struct {
+    int64_t b, l, d, w;
+    int32_t dilation;
+    float scale;           /* multiplies Q.K before the softmax                    */
+    int32_t in_dtype;      /* ollie_dtype, must be OLLIE_BF16                      */
+    int32_t out_dtype;     /* ollie_dtype of O                                     */
+} ollie_band_desc;
+
+/* ------------------------------------------------------------------ helpers */
+
+/* Output extent of the operator (transposed = 0: conv2d / dilated conv2d,
+ * 1: conv_transpose2d):
+ *   forward    ho = floor((h + 2*pad_h - dil_h*(r-1) - 1) / stride_h) + 1
+ *   transposed ho = (h-1)*stride_h - 2*pad_h + dil_h*(r-1) + out_pad_h + 1
+ * and likewise for wo.  Returns OLLIE_EINVAL on invalid geometry or an empty output. */
+int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, int64_t* wo);
+
+/* Bytes of workspace that derived_conv2d / derived_dilated_conv2d /
+ * derived_conv_transpose2d need: the instantiated scope Y [n*h*w][r*s*k] in fp32
+ * (or bf16 with OLLIE_Y_BF16).  Returns 0 for invalid geometry. */
+size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags);
+
+/* Bytes of workspace banded_bmm needs: 0 for the fused path; with OLLIE_BAND_STAGED,
+ * S [b][l][2w+1] fp32 followed (at a 256-byte aligned offset) by P [b][l][2w+1] bf16. */
+size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags);
+
+/* Message for the last failure on this thread ("" if none); valid until the next
+ * library call on this thread. */
+const char* ollie_last_error(void);
+
+/* Library version string. */
+const char* ollie_version(void);
+
+/* ------------------------------------------------------------- entry points */
+
+/* Convolution (cross-correlation, section 4.2 expression E1) with stride and zero
+ * padding, dilation 1, as a GEMM over all input pixels followed by the OffsetAdd
+ * eOperator (section 2, Fig. "optimization found"):
+ *   Y[m][(r*S+s)*K+k] = sum_c X[m][c] * Wt[r][s][k][c]
+ *   out[n][ho][wo][k] = sum_{r,s} [0 <= hi < h][0 <= wi < w] Y[(n*h+hi)*w+wi][(r*S+s)*K+k]
+ *   with hi = ho*stride_h - pad_h + r, wi = wo*stride_w - pad_w + s.
+ * x: X, wt: Wt, out: out (layouts above).  ws: workspace of at least
+ * ollie_conv_workspace_bytes(desc, 0, flags) bytes (holds Y).  flags: OLLIE_Y_BF16.
+ * Rejects dil != 1 (OLLIE_EINVAL; use derived_dilated_conv2d). */
+int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
+                   void* ws, size_t ws_bytes, uint32_t flags, void* stream);
+
+/* Dilated convolution as the same GEMM plus the dilated OffsetAdd: taps are spaced by
+ * the dilation, hi = ho*stride_h - pad_h + r*dil_h, wi = wo*stride_w - pad_w + s*dil_w;
+ * taps outside the image read the zero padding and are skipped (boundary tightening,
+ * section 4.2).  Same arguments as derived_conv2d; any dil >= 1. */
+int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt,
+                           void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                           void* stream);
+
+/* Transposed convolution (section 6.3): the GEMM runs on the unpadded input, then
+ * each output sums only the partials that land on it (selective add):
+ *   out[n][ho][wo][k] = sum_{r,s} [th >= 0, th % stride_h == 0, th/stride_h < h]
+ *                               [tw >= 0, tw % stride_w == 0, tw/stride_w < w]
+ *                       Y[(n*h + th/stride_h)*w + tw/stride_w][(r*S+s)*K+k]
+ *   with th = ho + pad_h - r*dil_h, tw = wo + pad_w - s*dil_w.
+ * Here c is the operator's input channel count and k its output channel count.
+ * Same arguments as derived_conv2d; ws sized with transposed = 1. */
+int derived_conv_transpose2d(const ollie_conv_desc* desc, const void* x, const void* wt,
+                             void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                             void* stream);
+
+/* Banded dilated batched matmul with row softmax (Longformer-style sliding window):
+ *   S[b][i][j] = scale * sum_e Q[b][i][e] * K0[b][t][e],  t = i + (j-w)*dilation
+ *   P[b][i][:] = softmax_j S[b][i][:]
+ *   O[b][i][e] = sum_j P[b][i][j] * V0[b][t][e]
+ * K0, V0 are K, V with rows outside [0,l) reading zero.  By default such entries keep
+ * S = 0 and take part in the softmax (zero mode); with OLLIE_BAND_MASK_INVALID they
+ * are left out (P = 0).  The dilated band is evaluated as `dilation` non-dilated bands
+ * over the row subsequences i = dilation*i' + rho (section 6.4).
+ * Default: one fused kernel, S and P never leave the chip, ws may be NULL and
+ * s_out must be NULL.  With OLLIE_BAND_STAGED: three kernels (G2BMM -> softmax
+ * eOperator -> band-times-dense) through fp32 S and bf16 P in ws; if s_out is not
+ * NULL, S [b][l][2w+1] fp32 is written there instead of into ws. */
+int banded_bmm(const ollie_band_desc* desc, const void* q, const void* k, const void* v,
+               void* o, float* s_out, void* ws, size_t ws_bytes, uint32_t flags,
+               void* stream);
+
+/* ------------------------------------------------- stage entry points (same kernels) */
+
+/* GEMM stage alone: Y[m][n] = sum_kk A[m][kk] * B[n][kk] (A [m][k], B [n][k], Y [m][n]).
+ * in_dtype F32 or BF16 (A and B); y_dtype F32 or BF16.  BF16 needs k % 8 == 0. */
+int ollie_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
+                  int32_t in_dtype, int32_t y_dtype, void* stream);
+
+/* eOperator alone: y is the scope Y [n*h*w][r*s*k] in y_dtype; out as in the
+ * descriptor.  transposed = 0: (dilated) OffsetAdd; 1: the transposed selective add. */
+int ollie_eop_gather(const ollie_conv_desc* desc, int transposed, const void* y,
+                     int32_t y_dtype, void* out, void* stream);
+
+/* Band stages alone (layouts as in banded_bmm):
+ *   g2bmm:   S fp32 [b][l][2w+1] from Q, K
+ *   softmax: P bf16 [b][l][2w+1] from S (flags: OLLIE_BAND_MASK_INVALID)
+ *   gbmm:    O from P and V */
+int ollie_band_g2bmm(const ollie_band_desc* desc, const void* q, const void* k, float* s,
+                     void* stream);
+int ollie_band_softmax(const ollie_band_desc* desc, const float* s, void* p, uint32_t flags,
+                       void* stream);
+int ollie_band_gbmm(const ollie_band_desc* desc, const void* p, const void* v, void* o,
+                    void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OLLIE_H */

@@ -1,0 +1,307 @@
+"""Python binding of the gfx950 derived-operator library (libollie.so, include/ollie.h).
+
+Argument marshalling only: every step of every operator runs in the library's HIP
+kernels.  torch provides device memory and the current HIP stream.  There is no CPU
+fallback: if libollie.so is missing or the tensors are not on a GPU, calls raise.
+
+Layouts (contiguous):
+  x   [n][h][w][c] (NHWC)          wt  [r][s][k][c]  (torch conv2d weight .permute(2,3,0,1),
+                                                     conv_transpose2d weight .permute(2,3,1,0))
+  out [n][ho][wo][k]
+  q, k, v, o [b][l][d]             s   [b][l][2w+1]
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libollie.so")
+
+OK, EINVAL, EDTYPE, EWORKSPACE, EALIGN, EHIP = range(6)
+F32, BF16 = 0, 1
+Y_BF16 = 1 << 1
+BAND_STAGED = 1 << 2
+BAND_MASK_INVALID = 1 << 3
+
+_STATUS_NAMES = {OK: "OLLIE_OK", EINVAL: "OLLIE_EINVAL", EDTYPE: "OLLIE_EDTYPE",
+                 EWORKSPACE: "OLLIE_EWORKSPACE", EALIGN: "OLLIE_EALIGN", EHIP: "OLLIE_EHIP"}
+
+EXPORTS = ("derived_conv2d", "derived_dilated_conv2d", "derived_conv_transpose2d", "banded_bmm",
+           "ollie_conv_out_hw", "ollie_conv_workspace_bytes", "ollie_band_workspace_bytes",
+           "ollie_last_error", "ollie_version", "ollie_gemm_nt", "ollie_eop_gather",
+           "ollie_band_g2bmm", "ollie_band_softmax", "ollie_band_gbmm")
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("c", ctypes.c_int64), ("h", ctypes.c_int64),
+                ("w", ctypes.c_int64), ("k", ctypes.c_int64), ("r", ctypes.c_int64),
+                ("s", ctypes.c_int64),
+                ("stride_h", ctypes.c_int32), ("stride_w", ctypes.c_int32),
+                ("pad_h", ctypes.c_int32), ("pad_w", ctypes.c_int32),
+                ("dil_h", ctypes.c_int32), ("dil_w", ctypes.c_int32),
+                ("out_pad_h", ctypes.c_int32), ("out_pad_w", ctypes.c_int32),
+                ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class BandDesc(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int64), ("l", ctypes.c_int64), ("d", ctypes.c_int64),
+                ("w", ctypes.c_int64), ("dilation", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class OllieError(RuntimeError):
+    def __init__(self, status: int, fn: str, msg: str):
+        super().__init__(f"{fn}: {_STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libollie.so (building it first only if it does not exist)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        from . import _build
+        _build.build()
+    lib = ctypes.CDLL(path)
+    p, i64, i32, u32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32,
+                            ctypes.c_size_t)
+    cdp, bdp = ctypes.POINTER(ConvDesc), ctypes.POINTER(BandDesc)
+    sig = {
+        "derived_conv2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
+        "derived_dilated_conv2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
+        "derived_conv_transpose2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
+        "banded_bmm": ([bdp, p, p, p, p, p, p, sz, u32, p], ctypes.c_int),
+        "ollie_conv_out_hw": ([cdp, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64)],
+                              ctypes.c_int),
+        "ollie_conv_workspace_bytes": ([cdp, ctypes.c_int, u32], sz),
+        "ollie_band_workspace_bytes": ([bdp, u32], sz),
+        "ollie_last_error": ([], ctypes.c_char_p),
+        "ollie_version": ([], ctypes.c_char_p),
+        "ollie_gemm_nt": ([i64, i64, i64, p, p, p, i32, i32, p], ctypes.c_int),
+        "ollie_eop_gather": ([cdp, ctypes.c_int, p, i32, p, p], ctypes.c_int),
+        "ollie_band_g2bmm": ([bdp, p, p, p, p], ctypes.c_int),
+        "ollie_band_softmax": ([bdp, p, p, u32, p], ctypes.c_int),
+        "ollie_band_gbmm": ([bdp, p, p, p, p], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(status: int, fn: str):
+    if status != OK:
+        raise OllieError(status, fn, load_library().ollie_last_error().decode())
+
+
+def _pair(v):
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return F32
+    if dt == torch.bfloat16:
+        return BF16
+    raise ValueError(f"unsupported dtype {dt}; use torch.float32 or torch.bfloat16")
+
+
+def _torch_dtype(code: int) -> torch.dtype:
+    return torch.bfloat16 if code == BF16 else torch.float32
+
+
+def _gpu(t: torch.Tensor, name: str):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (the library has no CPU path)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(dev) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def conv_desc(x_shape, wt_shape, stride=1, padding=0, dilation=1, output_padding=0,
+              in_dtype=torch.bfloat16, out_dtype=torch.float32) -> ConvDesc:
+    n, h, w, c = x_shape
+    r, s, k, c2 = wt_shape
+    if c != c2:
+        raise ValueError(f"x has {c} channels but wt expects {c2}")
+    (sh, sw), (ph, pw), (dh, dw), (oh, ow) = (_pair(stride), _pair(padding), _pair(dilation),
+                                              _pair(output_padding))
+    return ConvDesc(n, c, h, w, k, r, s, sh, sw, ph, pw, dh, dw, oh, ow,
+                    _dtype_code(in_dtype), _dtype_code(out_dtype))
+
+
+def conv_out_hw(desc: ConvDesc, transposed: bool):
+    ho, wo = ctypes.c_int64(), ctypes.c_int64()
+    _check(load_library().ollie_conv_out_hw(ctypes.byref(desc), int(transposed),
+                                            ctypes.byref(ho), ctypes.byref(wo)),
+           "ollie_conv_out_hw")
+    return ho.value, wo.value
+
+
+def conv_workspace_bytes(desc: ConvDesc, transposed: bool, flags: int = 0) -> int:
+    return int(load_library().ollie_conv_workspace_bytes(ctypes.byref(desc), int(transposed),
+                                                         flags))
+
+
+def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output_padding,
+          out_dtype, y_bf16, out, ws):
+    _gpu(x, "x")
+    _gpu(wt, "wt")
+    if x.dtype != wt.dtype:
+        raise ValueError("x and wt must have the same dtype")
+    desc = conv_desc(tuple(x.shape), tuple(wt.shape), stride, padding, dilation, output_padding,
+                     x.dtype, out_dtype)
+    flags = Y_BF16 if y_bf16 else 0
+    ho, wo = conv_out_hw(desc, transposed)
+    if out is None:
+        out = torch.empty((desc.n, ho, wo, desc.k), dtype=out_dtype, device=x.device)
+    else:
+        _gpu(out, "out")
+        if tuple(out.shape) != (desc.n, ho, wo, desc.k) or out.dtype != out_dtype:
+            raise ValueError("out has the wrong shape or dtype")
+    need = conv_workspace_bytes(desc, transposed, flags)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+    st = getattr(load_library(), entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out),
+                                        _ptr(ws), ws.numel() * ws.element_size(), flags,
+                                        _stream(x.device))
+    _check(st, entry)
+    return out
+
+
+def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=False,
+                   out=None, ws=None):
+    """Conv2d (dilation 1) as GEMM + OffsetAdd eOperator.  x [N,H,W,C], wt [R,S,K,C]."""
+    return _conv("derived_conv2d", False, x, wt, stride, padding, 1, 0, out_dtype, y_bf16,
+                 out, ws)
+
+
+def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,
+                           y_bf16=False, out=None, ws=None):
+    """Dilated Conv2d as GEMM + dilated OffsetAdd eOperator."""
+    return _conv("derived_dilated_conv2d", False, x, wt, stride, padding, dilation, 0,
+                 out_dtype, y_bf16, out, ws)
+
+
+def derived_conv_transpose2d(x, wt, stride=1, padding=0, output_padding=0, dilation=1,
+                             out_dtype=torch.float32, y_bf16=False, out=None, ws=None):
+    """ConvTranspose2d as GEMM on the unpadded input + selective-add eOperator.
+    x [N,H,W,C_in], wt [R,S,C_out,C_in]."""
+    return _conv("derived_conv_transpose2d", True, x, wt, stride, padding, dilation,
+                 output_padding, out_dtype, y_bf16, out, ws)
+
+
+def band_desc(q_shape, w, dilation, scale=1.0, out_dtype=torch.float32) -> BandDesc:
+    b, l, d = q_shape
+    return BandDesc(b, l, d, int(w), int(dilation), float(scale), BF16, _dtype_code(out_dtype))
+
+
+def band_workspace_bytes(desc: BandDesc, flags: int) -> int:
+    return int(load_library().ollie_band_workspace_bytes(ctypes.byref(desc), flags))
+
+
+def banded_bmm(q, k, v, w, dilation=1, scale=1.0, mask_invalid=False, staged=False,
+               out_dtype=torch.float32, return_s=False, out=None, ws=None, s_out=None):
+    """Banded dilated batched matmul + softmax + band-times-dense (q, k, v [B,L,64] bf16).
+
+    Returns O, or (O, S) when return_s (staged path only)."""
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        _gpu(t, name)
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{name} must be bfloat16")
+        if t.shape != q.shape:
+            raise ValueError("q, k, v must have the same shape")
+    desc = band_desc(tuple(q.shape), w, dilation, scale, out_dtype)
+    flags = (BAND_STAGED if staged or return_s else 0) | (BAND_MASK_INVALID if mask_invalid else 0)
+    if out is None:
+        out = torch.empty(tuple(q.shape), dtype=out_dtype, device=q.device)
+    if return_s and s_out is None:
+        s_out = torch.empty((desc.b, desc.l, 2 * desc.w + 1), dtype=torch.float32, device=q.device)
+    need = band_workspace_bytes(desc, flags)
+    if ws is None and need:
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load_library().banded_bmm(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                   _ptr(s_out), _ptr(ws), ws_bytes, flags, _stream(q.device))
+    _check(st, "banded_bmm")
+    return (out, s_out) if return_s else out
+
+
+# ------------------------------------------------------------------ stage entry points
+
+def gemm_nt(a, b, y_dtype=torch.float32, out=None):
+    """Y[m][n] = sum_k A[m][k] B[n][k] on the GEMM-stage kernel."""
+    _gpu(a, "a")
+    _gpu(b, "b")
+    m, kk = a.shape
+    n, kk2 = b.shape
+    if kk != kk2 or a.dtype != b.dtype:
+        raise ValueError("a and b must share k and dtype")
+    if out is None:
+        out = torch.empty((m, n), dtype=y_dtype, device=a.device)
+    st = load_library().ollie_gemm_nt(m, n, kk, _ptr(a), _ptr(b), _ptr(out), _dtype_code(a.dtype),
+                                      _dtype_code(out.dtype), _stream(a.device))
+    _check(st, "ollie_gemm_nt")
+    return out
+
+
+def eop_gather(desc: ConvDesc, transposed: bool, y, out=None):
+    """eOperator stage alone on a GEMM-stage scope y [n*h*w][r*s*k]."""
+    _gpu(y, "y")
+    ho, wo = conv_out_hw(desc, transposed)
+    if out is None:
+        out = torch.empty((desc.n, ho, wo, desc.k), dtype=_torch_dtype(desc.out_dtype),
+                          device=y.device)
+    st = load_library().ollie_eop_gather(ctypes.byref(desc), int(transposed), _ptr(y),
+                                         _dtype_code(y.dtype), _ptr(out), _stream(y.device))
+    _check(st, "ollie_eop_gather")
+    return out
+
+
+def band_g2bmm(q, k, w, dilation=1, scale=1.0, s=None):
+    desc = band_desc(tuple(q.shape), w, dilation, scale)
+    if s is None:
+        s = torch.empty((desc.b, desc.l, 2 * desc.w + 1), dtype=torch.float32, device=q.device)
+    _check(load_library().ollie_band_g2bmm(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(s),
+                                           _stream(q.device)), "ollie_band_g2bmm")
+    return s
+
+
+def band_softmax(s, w, dilation=1, mask_invalid=False, p=None):
+    b, l, nb = s.shape
+    desc = band_desc((b, l, 64), w, dilation)
+    if p is None:
+        p = torch.empty((b, l, nb), dtype=torch.bfloat16, device=s.device)
+    _check(load_library().ollie_band_softmax(ctypes.byref(desc), _ptr(s), _ptr(p),
+                                             BAND_MASK_INVALID if mask_invalid else 0,
+                                             _stream(s.device)), "ollie_band_softmax")
+    return p
+
+
+def band_gbmm(p, v, w, dilation=1, out_dtype=torch.float32, o=None):
+    desc = band_desc(tuple(v.shape), w, dilation, 1.0, out_dtype)
+    if o is None:
+        o = torch.empty(tuple(v.shape), dtype=out_dtype, device=v.device)
+    _check(load_library().ollie_band_gbmm(ctypes.byref(desc), _ptr(p), _ptr(v), _ptr(o),
+                                          _stream(v.device)), "ollie_band_gbmm")
+    return o
+
+
+def version() -> str:
+    return load_library().ollie_version().decode()

@@ -1,0 +1,339 @@
+// Host side of the C ABI declared in include/ollie.h: argument validation, output and
+// workspace sizing, and kernel launches on the caller's stream.  Every check runs
+// before the first HIP call, so invalid arguments never reach the device.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/ollie.h"
+#include "common.h"
+
+using namespace ollie;
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(OLLIE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool dtype_ok(int32_t d) { return d == OLLIE_F32 || d == OLLIE_BF16; }
+
+size_t dsize(int32_t d) { return d == OLLIE_BF16 ? 2 : 4; }
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;   // per-tensor element bound for 32-bit index math
+
+// Overflow-checked product of non-negative values; -1 if it exceeds 2^62.
+int64_t mul(int64_t a, int64_t b) {
+    if (a < 0 || b < 0) return -1;
+    if (a != 0 && b > ((int64_t)1 << 62) / a) return -1;
+    return a * b;
+}
+
+int check_conv_geom(const ollie_conv_desc* d, int transposed, int64_t* ho, int64_t* wo) {
+    if (!d) return fail(OLLIE_EINVAL, "desc is NULL");
+    if (d->n < 1 || d->c < 1 || d->h < 1 || d->w < 1 || d->k < 1 || d->r < 1 || d->s < 1)
+        return fail(OLLIE_EINVAL, "n, c, h, w, k, r, s must all be >= 1");
+    if (d->stride_h < 1 || d->stride_w < 1) return fail(OLLIE_EINVAL, "stride must be >= 1");
+    if (d->dil_h < 1 || d->dil_w < 1) return fail(OLLIE_EINVAL, "dilation must be >= 1");
+    if (d->pad_h < 0 || d->pad_w < 0) return fail(OLLIE_EINVAL, "padding must be >= 0");
+    if (transposed) {
+        int mh = d->stride_h > d->dil_h ? d->stride_h : d->dil_h;
+        int mw = d->stride_w > d->dil_w ? d->stride_w : d->dil_w;
+        if (d->out_pad_h < 0 || d->out_pad_w < 0 || d->out_pad_h >= mh || d->out_pad_w >= mw)
+            return fail(OLLIE_EINVAL, "out_pad must satisfy 0 <= out_pad < max(stride, dilation)");
+    } else if (d->out_pad_h != 0 || d->out_pad_w != 0) {
+        return fail(OLLIE_EINVAL, "out_pad is only meaningful for conv_transpose2d");
+    }
+    int64_t oh, ow;
+    if (transposed) {
+        oh = (d->h - 1) * d->stride_h - 2 * (int64_t)d->pad_h + (int64_t)d->dil_h * (d->r - 1) +
+             d->out_pad_h + 1;
+        ow = (d->w - 1) * d->stride_w - 2 * (int64_t)d->pad_w + (int64_t)d->dil_w * (d->s - 1) +
+             d->out_pad_w + 1;
+    } else {
+        int64_t sh = d->h + 2 * (int64_t)d->pad_h - (int64_t)d->dil_h * (d->r - 1) - 1;
+        int64_t sw = d->w + 2 * (int64_t)d->pad_w - (int64_t)d->dil_w * (d->s - 1) - 1;
+        oh = sh < 0 ? 0 : sh / d->stride_h + 1;
+        ow = sw < 0 ? 0 : sw / d->stride_w + 1;
+    }
+    if (oh < 1 || ow < 1) return fail(OLLIE_EINVAL, "output would be empty (ho=%lld, wo=%lld)",
+                                      (long long)oh, (long long)ow);
+    int64_t m = mul(mul(d->n, d->h), d->w);
+    int64_t nc = mul(mul(d->r, d->s), d->k);
+    int64_t outn = mul(mul(mul(d->n, oh), ow), d->k);
+    int64_t yel = mul(m, nc);
+    if (m < 0 || nc < 0 || outn < 0 || yel < 0 || mul(m, d->c) < 0 || mul(nc, d->c) < 0)
+        return fail(OLLIE_EINVAL, "sizes overflow 64-bit arithmetic");
+    if (m >= kMaxElems || nc >= kMaxElems || outn >= kMaxElems)
+        return fail(OLLIE_EINVAL, "n*h*w, r*s*k and the output size must each be < 2^31");
+    *ho = oh;
+    *wo = ow;
+    return OLLIE_OK;
+}
+
+ConvGeom conv_geom(const ollie_conv_desc* d, int64_t ho, int64_t wo) {
+    ConvGeom g;
+    g.n = d->n; g.c = d->c; g.h = d->h; g.w = d->w; g.k = d->k; g.r = d->r; g.s = d->s;
+    g.ho = ho; g.wo = wo;
+    g.sh = d->stride_h; g.sw = d->stride_w; g.ph = d->pad_h; g.pw = d->pad_w;
+    g.dh = d->dil_h; g.dw = d->dil_w;
+    return g;
+}
+
+size_t conv_ws(const ollie_conv_desc* d, uint32_t flags) {
+    return (size_t)(d->n * d->h * d->w) * (size_t)(d->r * d->s * d->k) *
+           ((flags & OLLIE_Y_BF16) ? 2 : 4);
+}
+
+int check_gemm(int64_t m, int64_t n, int64_t k, const void* a, const void* b, const void* y,
+               int32_t in_dtype, int32_t y_dtype) {
+    if (m < 1 || n < 1 || k < 1) return fail(OLLIE_EINVAL, "m, n, k must be >= 1");
+    if (mul(m, k) < 0 || mul(n, k) < 0 || mul(m, n) < 0)
+        return fail(OLLIE_EINVAL, "sizes overflow 64-bit arithmetic");
+    if (m >= kMaxElems || n >= kMaxElems) return fail(OLLIE_EINVAL, "m and n must be < 2^31");
+    if (!a || !b || !y) return fail(OLLIE_EINVAL, "null tensor pointer");
+    if (!dtype_ok(in_dtype) || !dtype_ok(y_dtype)) return fail(OLLIE_EDTYPE, "unknown dtype");
+    if (!aligned16(a) || !aligned16(b) || !aligned16(y))
+        return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    if (in_dtype == OLLIE_BF16 && (k % 8) != 0)
+        return fail(OLLIE_EALIGN, "bf16 operands need k %% 8 == 0 (16-byte rows), got k=%lld",
+                    (long long)k);
+    return OLLIE_OK;
+}
+
+int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
+                void* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+    int64_t ho, wo;
+    int st = check_conv_geom(d, transposed, &ho, &wo);
+    if (st) return st;
+    if (flags & ~(uint32_t)OLLIE_Y_BF16) return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
+    if (!x || !wt || !out || !ws) return fail(OLLIE_EINVAL, "null tensor or workspace pointer");
+    if (!dtype_ok(d->in_dtype) || !dtype_ok(d->out_dtype))
+        return fail(OLLIE_EDTYPE, "in_dtype/out_dtype must be OLLIE_F32 or OLLIE_BF16");
+    size_t need = conv_ws(d, flags);
+    if (ws_bytes < need)
+        return fail(OLLIE_EWORKSPACE, "workspace too small: need %zu bytes, got %zu", need,
+                    ws_bytes);
+    if (!aligned16(x) || !aligned16(wt) || !aligned16(out) || !aligned16(ws))
+        return fail(OLLIE_EALIGN, "tensor and workspace pointers must be 16-byte aligned");
+    int64_t m = d->n * d->h * d->w, nc = d->r * d->s * d->k;
+    st = check_gemm(m, nc, d->c, x, wt, ws, d->in_dtype,
+                    (flags & OLLIE_Y_BF16) ? OLLIE_BF16 : OLLIE_F32);
+    if (st) return st;
+    hipStream_t s = (hipStream_t)stream;
+    const int y_bf16 = (flags & OLLIE_Y_BF16) ? 1 : 0;
+    hipError_t e = launch_gemm_nt(m, nc, d->c, x, wt, ws, d->in_dtype == OLLIE_BF16, y_bf16, s);
+    if (e != hipSuccess) return hip_fail(e, "GEMM stage launch");
+    e = launch_eop_gather(conv_geom(d, ho, wo), transposed, ws, y_bf16, out,
+                          d->out_dtype == OLLIE_BF16, s);
+    if (e != hipSuccess) return hip_fail(e, "eOperator launch");
+    return OLLIE_OK;
+}
+
+int check_band(const ollie_band_desc* d) {
+    if (!d) return fail(OLLIE_EINVAL, "desc is NULL");
+    if (d->b < 1 || d->l < 1 || d->w < 0 || d->dilation < 1)
+        return fail(OLLIE_EINVAL, "need b >= 1, l >= 1, w >= 0, dilation >= 1");
+    if (d->d != 64) return fail(OLLIE_EINVAL, "head dimension d must be 64, got %lld",
+                                (long long)d->d);
+    if (d->b > 65535 || d->dilation > 65535)
+        return fail(OLLIE_EINVAL, "b and dilation must be <= 65535");
+    if (d->in_dtype != OLLIE_BF16) return fail(OLLIE_EDTYPE, "Q, K, V must be bf16");
+    if (!dtype_ok(d->out_dtype)) return fail(OLLIE_EDTYPE, "out_dtype must be F32 or BF16");
+    int64_t nb = mul(2, d->w) + 1;
+    if (mul(mul(d->b, d->l), nb) < 0 || mul(mul(d->b, d->l), d->d) < 0 || d->w > ((int64_t)1 << 30))
+        return fail(OLLIE_EINVAL, "sizes overflow 64-bit arithmetic");
+    if (mul(d->b, d->l) >= kMaxElems) return fail(OLLIE_EINVAL, "b*l must be < 2^31");
+    return OLLIE_OK;
+}
+
+BandGeom band_geom(const ollie_band_desc* d) {
+    BandGeom g;
+    g.b = d->b; g.l = d->l; g.d = d->d; g.w = d->w; g.dil = d->dilation; g.scale = d->scale;
+    return g;
+}
+
+size_t band_s_bytes(const ollie_band_desc* d) {
+    return (size_t)(d->b * d->l) * (size_t)(2 * d->w + 1) * 4;
+}
+size_t band_p_offset(const ollie_band_desc* d) { return (band_s_bytes(d) + 255) & ~(size_t)255; }
+size_t band_p_bytes(const ollie_band_desc* d) {
+    return (size_t)(d->b * d->l) * (size_t)(2 * d->w + 1) * 2;
+}
+
+constexpr int64_t kSoftmaxMaxBand = 16 * 64;   // register-resident row length of the staged softmax
+
+}  // namespace
+
+extern "C" {
+
+const char* ollie_last_error(void) { return g_err; }
+
+const char* ollie_version(void) { return "ollie-mi355x 0.1.0 (gfx950)"; }
+
+int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, int64_t* wo) {
+    g_err[0] = 0;
+    if (!ho || !wo) return fail(OLLIE_EINVAL, "ho/wo pointers are NULL");
+    return check_conv_geom(desc, transposed ? 1 : 0, ho, wo);
+}
+
+size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags) {
+    int64_t ho, wo;
+    if (check_conv_geom(desc, transposed ? 1 : 0, &ho, &wo)) return 0;
+    return conv_ws(desc, flags);
+}
+
+size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags) {
+    if (check_band(desc)) return 0;
+    if (!(flags & OLLIE_BAND_STAGED)) return 0;
+    return band_p_offset(desc) + band_p_bytes(desc);
+}
+
+int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
+                   void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+    g_err[0] = 0;
+    if (desc && (desc->dil_h != 1 || desc->dil_w != 1))
+        return fail(OLLIE_EINVAL, "derived_conv2d takes dilation 1; use derived_dilated_conv2d");
+    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, stream);
+}
+
+int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt,
+                           void* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+    g_err[0] = 0;
+    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, stream);
+}
+
+int derived_conv_transpose2d(const ollie_conv_desc* desc, const void* x, const void* wt,
+                             void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                             void* stream) {
+    g_err[0] = 0;
+    return conv_common(desc, 1, x, wt, out, ws, ws_bytes, flags, stream);
+}
+
+int banded_bmm(const ollie_band_desc* desc, const void* q, const void* k, const void* v,
+               void* o, float* s_out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+    g_err[0] = 0;
+    int st = check_band(desc);
+    if (st) return st;
+    if (flags & ~(uint32_t)(OLLIE_BAND_STAGED | OLLIE_BAND_MASK_INVALID))
+        return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
+    if (!q || !k || !v || !o) return fail(OLLIE_EINVAL, "null tensor pointer");
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+        return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    const int mask = (flags & OLLIE_BAND_MASK_INVALID) ? 1 : 0;
+    const int o_bf16 = desc->out_dtype == OLLIE_BF16;
+    hipStream_t s = (hipStream_t)stream;
+    BandGeom g = band_geom(desc);
+    if (!(flags & OLLIE_BAND_STAGED)) {
+        if (s_out) return fail(OLLIE_EINVAL, "s_out needs OLLIE_BAND_STAGED");
+        hipError_t e = launch_band_fused(g, q, k, v, o, o_bf16, mask, s);
+        if (e != hipSuccess) return hip_fail(e, "fused band launch");
+        return OLLIE_OK;
+    }
+    if (2 * desc->w + 1 > kSoftmaxMaxBand)
+        return fail(OLLIE_EINVAL, "staged path needs 2w+1 <= %lld", (long long)kSoftmaxMaxBand);
+    size_t need = band_p_offset(desc) + band_p_bytes(desc);
+    if (!ws) return fail(OLLIE_EINVAL, "staged path needs a workspace");
+    if (ws_bytes < need)
+        return fail(OLLIE_EWORKSPACE, "workspace too small: need %zu bytes, got %zu", need,
+                    ws_bytes);
+    if (!aligned16(ws) || (s_out && !aligned16(s_out)))
+        return fail(OLLIE_EALIGN, "workspace and s_out must be 16-byte aligned");
+    float* sbuf = s_out ? s_out : (float*)ws;
+    void* pbuf = (char*)ws + band_p_offset(desc);
+    hipError_t e = launch_band_g2bmm(g, q, k, sbuf, s);
+    if (e != hipSuccess) return hip_fail(e, "G2BMM launch");
+    e = launch_band_softmax(g, sbuf, pbuf, mask, s);
+    if (e != hipSuccess) return hip_fail(e, "softmax launch");
+    e = launch_band_gbmm(g, pbuf, v, o, o_bf16, s);
+    if (e != hipSuccess) return hip_fail(e, "GBMM launch");
+    return OLLIE_OK;
+}
+
+int ollie_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
+                  int32_t in_dtype, int32_t y_dtype, void* stream) {
+    g_err[0] = 0;
+    int st = check_gemm(m, n, k, a, b, y, in_dtype, y_dtype);
+    if (st) return st;
+    hipError_t e = launch_gemm_nt(m, n, k, a, b, y, in_dtype == OLLIE_BF16,
+                                  y_dtype == OLLIE_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+    return OLLIE_OK;
+}
+
+int ollie_eop_gather(const ollie_conv_desc* desc, int transposed, const void* y,
+                     int32_t y_dtype, void* out, void* stream) {
+    g_err[0] = 0;
+    int64_t ho, wo;
+    int st = check_conv_geom(desc, transposed ? 1 : 0, &ho, &wo);
+    if (st) return st;
+    if (!y || !out) return fail(OLLIE_EINVAL, "null tensor pointer");
+    if (!dtype_ok(y_dtype) || !dtype_ok(desc->out_dtype)) return fail(OLLIE_EDTYPE, "unknown dtype");
+    if (!aligned16(y) || !aligned16(out))
+        return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    hipError_t e = launch_eop_gather(conv_geom(desc, ho, wo), transposed ? 1 : 0, y,
+                                     y_dtype == OLLIE_BF16, out, desc->out_dtype == OLLIE_BF16,
+                                     (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "eOperator launch");
+    return OLLIE_OK;
+}
+
+int ollie_band_g2bmm(const ollie_band_desc* desc, const void* q, const void* k, float* s,
+                     void* stream) {
+    g_err[0] = 0;
+    int st = check_band(desc);
+    if (st) return st;
+    if (!q || !k || !s) return fail(OLLIE_EINVAL, "null tensor pointer");
+    if (!aligned16(q) || !aligned16(k) || !aligned16(s))
+        return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    hipError_t e = launch_band_g2bmm(band_geom(desc), q, k, s, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "G2BMM launch");
+    return OLLIE_OK;
+}
+
+int ollie_band_softmax(const ollie_band_desc* desc, const float* s, void* p, uint32_t flags,
+                       void* stream) {
+    g_err[0] = 0;
+    int st = check_band(desc);
+    if (st) return st;
+    if (flags & ~(uint32_t)OLLIE_BAND_MASK_INVALID)
+        return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
+    if (!s || !p) return fail(OLLIE_EINVAL, "null tensor pointer");
+    if (2 * desc->w + 1 > kSoftmaxMaxBand)
+        return fail(OLLIE_EINVAL, "softmax stage needs 2w+1 <= %lld", (long long)kSoftmaxMaxBand);
+    if (!aligned16(s) || !aligned16(p))
+        return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    hipError_t e = launch_band_softmax(band_geom(desc), s, p,
+                                       (flags & OLLIE_BAND_MASK_INVALID) ? 1 : 0,
+                                       (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "softmax launch");
+    return OLLIE_OK;
+}
+
+int ollie_band_gbmm(const ollie_band_desc* desc, const void* p, const void* v, void* o,
+                    void* stream) {
+    g_err[0] = 0;
+    int st = check_band(desc);
+    if (st) return st;
+    if (!p || !v || !o) return fail(OLLIE_EINVAL, "null tensor pointer");
+    if (!aligned16(p) || !aligned16(v) || !aligned16(o))
+        return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    hipError_t e = launch_band_gbmm(band_geom(desc), p, v, o, desc->out_dtype == OLLIE_BF16,
+                                    (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "GBMM launch");
+    return OLLIE_OK;
+}
+
+}  // extern "C"

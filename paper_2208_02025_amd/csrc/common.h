@@ -1,0 +1,94 @@
+// Internal helpers shared by the gfx950 kernels and the host dispatch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ollie {
+
+typedef uint16_t bf16_t;                                         // raw bfloat16 bits
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));       // MFMA operand (8 x bf16)
+typedef float f32x4 __attribute__((ext_vector_type(4)));         // 16x16 MFMA accumulator
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));      // 16-byte raw chunk
+
+// float -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
+        return (bf16_t)((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf2f(bf16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Store helpers for fp32 / bf16 outputs.
+template <typename T> struct Out;
+template <> struct Out<float> {
+    static __device__ __forceinline__ void put(float* p, float v) { *p = v; }
+    static __device__ __forceinline__ void put4(float* p, f32x4 v) {
+        *reinterpret_cast<f32x4*>(p) = v;
+    }
+};
+template <> struct Out<bf16_t> {
+    static __device__ __forceinline__ void put(bf16_t* p, float v) { *p = f2bf(v); }
+    static __device__ __forceinline__ void put4(bf16_t* p, f32x4 v) {
+        uint32_t lo = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+        uint32_t hi = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+        *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+    }
+};
+
+// Load helpers: 4 consecutive values widened to fp32.
+template <typename T> struct In;
+template <> struct In<float> {
+    static __device__ __forceinline__ float get(const float* p) { return *p; }
+    static __device__ __forceinline__ f32x4 get4(const float* p) {
+        return *reinterpret_cast<const f32x4*>(p);
+    }
+};
+template <> struct In<bf16_t> {
+    static __device__ __forceinline__ float get(const bf16_t* p) { return bf2f(*p); }
+    static __device__ __forceinline__ f32x4 get4(const bf16_t* p) {
+        uint2 u = *reinterpret_cast<const uint2*>(p);
+        f32x4 r;
+        r[0] = __uint_as_float(u.x << 16);
+        r[1] = __uint_as_float(u.x & 0xffff0000u);
+        r[2] = __uint_as_float(u.y << 16);
+        r[3] = __uint_as_float(u.y & 0xffff0000u);
+        return r;
+    }
+};
+
+// ---------------------------------------------------------------- launchers
+// Each returns the hipError_t of the launch.
+
+hipError_t launch_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b,
+                          void* y, int in_bf16, int y_bf16, hipStream_t stream);
+
+struct ConvGeom {
+    int64_t n, c, h, w, k, r, s, ho, wo;
+    int32_t sh, sw, ph, pw, dh, dw;
+};
+
+hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, int y_bf16,
+                             void* out, int out_bf16, hipStream_t stream);
+
+struct BandGeom {
+    int64_t b, l, d, w;
+    int32_t dil;
+    float scale;
+};
+
+hipError_t launch_band_g2bmm(const BandGeom& g, const void* q, const void* k, float* s,
+                             hipStream_t stream);
+hipError_t launch_band_softmax(const BandGeom& g, const float* s, void* p, int mask,
+                               hipStream_t stream);
+hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, void* o,
+                            int o_bf16, hipStream_t stream);
+hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
+                             void* o, int o_bf16, int mask, hipStream_t stream);
+
+}  // namespace ollie

@@ -1,0 +1,189 @@
+"""CPU-only checks of the C ABI: the library loads, exports every function that
+include/ollie.h declares, and rejects invalid arguments with the documented status
+before touching the GPU (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2208_02025_amd as ol
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ollie.h")
+
+# Fake, never-dereferenced device addresses: validation fails before any HIP call.
+A16 = ctypes.c_void_p(0x10000)
+B16 = ctypes.c_void_p(0x20000)
+C16 = ctypes.c_void_p(0x30000)
+W16 = ctypes.c_void_p(0x40000)
+MIS = ctypes.c_void_p(0x10008)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ol.load_library()
+
+
+def test_header_declares_the_four_entry_points():
+    names = header_functions()
+    for n in ("derived_conv2d", "derived_conv_transpose2d", "derived_dilated_conv2d",
+              "banded_bmm"):
+        assert n in names
+
+
+def test_library_exports_every_declared_function(lib):
+    names = header_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in ollie.h but not exported"
+    assert set(names) == set(ol.EXPORTS)
+
+
+def test_version(lib):
+    assert "gfx950" in ol.version()
+
+
+def conv(n=1, c=16, h=14, w=14, k=16, r=3, s=3, stride=1, pad=1, dil=1, op=0,
+         in_dtype=ol.BF16, out_dtype=ol.F32):
+    return ol.ConvDesc(n, c, h, w, k, r, s, stride, stride, pad, pad, dil, dil, op, op,
+                       in_dtype, out_dtype)
+
+
+def call_conv(lib, entry, d, x=A16, wt=B16, out=C16, ws=W16, ws_bytes=None, flags=0):
+    if ws_bytes is None:
+        ws_bytes = 1 << 40
+    st = getattr(lib, entry)(ctypes.byref(d) if d is not None else None, x, wt, out, ws,
+                             ws_bytes, flags, None)
+    return st, lib.ollie_last_error().decode()
+
+
+@pytest.mark.parametrize("entry", ["derived_conv2d", "derived_dilated_conv2d",
+                                   "derived_conv_transpose2d"])
+def test_conv_error_paths(lib, entry):
+    tr = entry == "derived_conv_transpose2d"
+    good_stride = 2 if tr else 1
+    cases = [
+        (None, {}, ol.EINVAL),
+        (conv(n=0), {}, ol.EINVAL),
+        (conv(c=0), {}, ol.EINVAL),
+        (conv(stride=0), {}, ol.EINVAL),
+        (conv(dil=0), {}, ol.EINVAL),
+        (conv(pad=-1), {}, ol.EINVAL),
+        (conv(in_dtype=7), {}, ol.EDTYPE),
+        (conv(out_dtype=3, stride=good_stride), {}, ol.EDTYPE),
+        (conv(stride=good_stride), {"x": None}, ol.EINVAL),
+        (conv(stride=good_stride), {"ws": None}, ol.EINVAL),
+        (conv(stride=good_stride), {"ws_bytes": 10}, ol.EWORKSPACE),
+        (conv(stride=good_stride), {"out": MIS}, ol.EALIGN),
+        (conv(c=12, stride=good_stride), {}, ol.EALIGN),          # bf16 rows not 16-byte multiples
+        (conv(stride=good_stride), {"flags": 1 << 9}, ol.EINVAL),
+        (conv(n=1 << 40, stride=good_stride), {}, ol.EINVAL),     # overflow
+    ]
+    if tr:
+        cases += [(conv(stride=2, op=2), {}, ol.EINVAL),          # out_pad >= max(stride, dil)
+                  (conv(stride=1, op=1), {}, ol.EINVAL),
+                  (conv(h=1, w=1, r=1, s=1, stride=1, pad=1), {}, ol.EINVAL)]   # empty output
+    else:
+        cases += [(conv(op=1), {}, ol.EINVAL),                    # out_pad on a forward conv
+                  (conv(h=2, w=2, r=5, s=5, pad=0), {}, ol.EINVAL)]           # empty output
+    if entry == "derived_conv2d":
+        cases.append((conv(dil=2, pad=2), {}, ol.EINVAL))
+    for d, kw, want in cases:
+        st, msg = call_conv(lib, entry, d, **kw)
+        assert st == want, (entry, kw, msg)
+        assert msg, "every failure sets a message"
+
+
+def test_conv_out_hw_and_workspace(lib):
+    d = conv(n=16, c=256, k=256)                                  # 3x3 conv, 14x14, pad 1
+    assert ol.conv_out_hw(d, False) == (14, 14)
+    assert ol.conv_workspace_bytes(d, False) == 16 * 14 * 14 * 9 * 256 * 4
+    assert ol.conv_workspace_bytes(d, False, ol.Y_BF16) == 16 * 14 * 14 * 9 * 256 * 2
+    d = conv(n=16, c=512, h=8, w=8, k=256, r=4, s=4, stride=2, pad=1)
+    assert ol.conv_out_hw(d, True) == (16, 16)
+    d = conv(n=1, c=512, h=96, w=128, k=512, pad=2, dil=2)
+    assert ol.conv_out_hw(d, False) == (96, 128)
+    with pytest.raises(ol.OllieError):
+        ol.conv_out_hw(conv(h=2, w=2, r=5, s=5, pad=0), False)
+    assert ol.conv_workspace_bytes(conv(n=0), False) == 0
+
+
+def band(b=2, l=64, d=64, w=4, dil=2, in_dtype=ol.BF16, out_dtype=ol.F32):
+    return ol.BandDesc(b, l, d, w, dil, 1.0, in_dtype, out_dtype)
+
+
+def test_band_error_paths(lib):
+    def call(d, q=A16, s_out=None, ws=None, ws_bytes=0, flags=0, o=C16):
+        st = lib.banded_bmm(ctypes.byref(d), q, B16, W16, o, s_out, ws, ws_bytes, flags, None)
+        return st, lib.ollie_last_error().decode()
+
+    cases = [
+        (band(d=32), {}, ol.EINVAL),
+        (band(b=0), {}, ol.EINVAL),
+        (band(l=0), {}, ol.EINVAL),
+        (band(w=-1), {}, ol.EINVAL),
+        (band(dil=0), {}, ol.EINVAL),
+        (band(in_dtype=ol.F32), {}, ol.EDTYPE),
+        (band(out_dtype=9), {}, ol.EDTYPE),
+        (band(), {"q": None}, ol.EINVAL),
+        (band(), {"o": MIS}, ol.EALIGN),
+        (band(), {"s_out": C16}, ol.EINVAL),                        # s_out needs the staged path
+        (band(), {"flags": 1 << 7}, ol.EINVAL),
+        (band(), {"flags": ol.BAND_STAGED}, ol.EINVAL),             # staged without workspace
+        (band(), {"flags": ol.BAND_STAGED, "ws": W16, "ws_bytes": 100}, ol.EWORKSPACE),
+        (band(w=600), {"flags": ol.BAND_STAGED, "ws": W16, "ws_bytes": 1 << 40}, ol.EINVAL),
+    ]
+    for d, kw, want in cases:
+        st, msg = call(d, **kw)
+        assert st == want, (kw, msg)
+        assert msg
+
+
+def test_band_workspace_bytes(lib):
+    d = band(b=96, l=4096, w=256, dil=2)
+    assert ol.band_workspace_bytes(d, 0) == 0
+    s_bytes = 96 * 4096 * 513 * 4
+    p_off = (s_bytes + 255) // 256 * 256
+    assert ol.band_workspace_bytes(d, ol.BAND_STAGED) == p_off + 96 * 4096 * 513 * 2
+
+
+def test_gemm_error_paths(lib):
+    def call(m=64, n=64, k=64, a=A16, b=B16, y=C16, it=ol.BF16, yt=ol.F32):
+        return lib.ollie_gemm_nt(m, n, k, a, b, y, it, yt, None)
+
+    assert call(m=0) == ol.EINVAL
+    assert call(k=-1) == ol.EINVAL
+    assert call(a=None) == ol.EINVAL
+    assert call(it=4) == ol.EDTYPE
+    assert call(y=MIS) == ol.EALIGN
+    assert call(k=20) == ol.EALIGN                                  # bf16 needs k % 8 == 0
+    assert call(m=1 << 40, k=1 << 30) == ol.EINVAL
+
+
+def test_stage_error_paths(lib):
+    d = conv()
+    assert lib.ollie_eop_gather(ctypes.byref(d), 0, None, ol.F32, C16, None) == ol.EINVAL
+    assert lib.ollie_eop_gather(ctypes.byref(d), 0, A16, 5, C16, None) == ol.EDTYPE
+    bd = band()
+    assert lib.ollie_band_g2bmm(ctypes.byref(bd), A16, None, C16, None) == ol.EINVAL
+    assert lib.ollie_band_softmax(ctypes.byref(bd), A16, MIS, 0, None) == ol.EALIGN
+    assert lib.ollie_band_softmax(ctypes.byref(bd), A16, C16, 1 << 5, None) == ol.EINVAL
+    assert lib.ollie_band_gbmm(ctypes.byref(band(d=16)), A16, B16, C16, None) == ol.EINVAL
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 4, 4, 8, dtype=torch.bfloat16)
+    wt = torch.zeros(3, 3, 8, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        ol.derived_conv2d(x, wt, 1, 1)
+    q = torch.zeros(1, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        ol.banded_bmm(q, q, q, 2, 1)
