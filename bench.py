@@ -217,42 +217,34 @@ def main():
 
 
 def cpu_baseline(conv_ops, bwl):
-    """The oracle (as it stands) on a bounded sample of one step: all outputs of the
-    two small convolutions, a seeded quarter of the dilated convolution's outputs and a
-    seeded 1/32 of the band rows; value = algorithmic flops of the sample / CPU time."""
-    import numpy as np
+    """The oracle (as it stands) on one whole step of the same workloads: every output
+    of the three convolutions and every row of the band (about 10-20 s on a 16-core
+    host); value = the step's algorithmic flops / CPU time."""
     import oracle
     import synth
 
     flops = 0.0
     secs = 0.0
-    rng = np.random.default_rng(0)
     for op in conv_ops:
         wl = op["wl"]
         x, wt = synth.conv_inputs(wl)
-        ho, wo = op["out"].shape[1:3]
-        n_out = wl.n * ho * wo * wl.k
-        frac = 1.0 if wl.cfg != 4 else 0.25
-        idx = None if frac == 1.0 else np.sort(rng.choice(n_out, int(n_out * frac), replace=False))
         t0 = time.perf_counter()
         if wl.transposed:
-            oracle.conv_transpose2d(x, wt, wl.stride, wl.pad, wl.dil, wl.out_pad, idx=idx)
+            oracle.conv_transpose2d(x, wt, wl.stride, wl.pad, wl.dil, wl.out_pad)
         else:
-            oracle.conv2d(x, wt, wl.stride, wl.pad, wl.dil, idx=idx)
+            oracle.conv2d(x, wt, wl.stride, wl.pad, wl.dil)
         secs += time.perf_counter() - t0
-        flops += op["flops"] * frac
+        flops += op["flops"]
     q, k, v = synth.band_inputs(bwl)
-    n_rows = bwl.b * bwl.l
-    rows = np.sort(rng.choice(n_rows, n_rows // 32, replace=False))
     t0 = time.perf_counter()
-    oracle.band(q, k, v, bwl.w, bwl.dilation, bwl.scale, bwl.mask_invalid, rows=rows,
-                want_s=False, want_p=False)
+    oracle.band(q, k, v, bwl.w, bwl.dilation, bwl.scale, bwl.mask_invalid, want_s=False,
+                want_p=False)
     secs += time.perf_counter() - t0
-    flops += band_flops(bwl) * len(rows) / n_rows
+    flops += band_flops(bwl)
     return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle", "seconds": round(secs, 2),
-            "sample": "all outputs of the conv3x3 and convT workloads, 25% of the dilated "
-                      "conv outputs, 1/32 of the band rows (seeded); flops scaled to the sample"}
+            "sample": "one whole step: all outputs of the conv3x3, convT and dilated conv "
+                      "workloads and all 393216 band rows"}
 
 
 if __name__ == "__main__":
