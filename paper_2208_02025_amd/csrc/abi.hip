@@ -156,6 +156,9 @@ int check_band(const ollie_band_desc* d) {
     if (mul(mul(d->b, d->l), nb) < 0 || mul(mul(d->b, d->l), d->d) < 0 || d->w > ((int64_t)1 << 30))
         return fail(OLLIE_EINVAL, "sizes overflow 64-bit arithmetic");
     if (mul(d->b, d->l) >= kMaxElems) return fail(OLLIE_EINVAL, "b*l must be < 2^31");
+    const int64_t tiles = ((d->l + d->dilation - 1) / d->dilation + 63) / 64;
+    if (mul(mul(tiles, d->dilation), d->b) >= kMaxElems)
+        return fail(OLLIE_EINVAL, "too many (batch, residue, 64-row) tiles");
     return OLLIE_OK;
 }
 

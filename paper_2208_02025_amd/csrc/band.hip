@@ -12,13 +12,16 @@
 // q0 + 16*wv .. +15 and, for each 64-key block, computes the transposed score block
 // S^T[t][q] = K[t] . Q[q] with v_mfma_f32_16x16x32_bf16 (A operand = key rows,
 // B operand = query rows).  Lane l then holds the scores of query q0+16*wv+l%16 for
-// keys 16*ft + 4*(l/16) + v (ft, v in 0..3) -- every value of a lane belongs to one
+// keys 16*ft + 4*(l/16) + v (ft, v in 0..3): every value of a lane belongs to one
 // query, so softmax statistics stay per lane until a final 4-lane reduction.
 //
 // For P*V the contraction runs over keys.  The MFMA's k-slots are assigned so that
 // lane group g = l/16 of a 32-key half h supplies keys 32h + {4g..4g+3, 16+4g..16+4g+3}:
-// exactly the keys the lane already holds in registers.  The V^T operand is read from
-// an LDS copy of the value block stored transposed, with the same key order.
+// exactly the keys the lane already holds in registers.  The V^T operand comes from a
+// row-major LDS copy of the value block through ds_read_b64_tr_b16, whose lane i of
+// each 16-lane group receives element i%4 of the 8-byte rows addressed by lanes
+// i/4 + 4j (j = 0..3): lanes address rows (keys) and 4-column slices, the hardware
+// returns one column (value dimension) across four keys.
 #include "common.h"
 
 namespace ollie {
@@ -27,81 +30,97 @@ namespace {
 
 constexpr int kD = 64;        // head dimension
 constexpr int kT = 64;        // queries per tile and keys per block
-constexpr int kVtLd = kT + 4; // row stride (elements) of the transposed V block in LDS
+constexpr int kVLd = kD + 8;  // row stride (elements) of the value block in LDS
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 struct Tile {
-    int64_t b;      // batch index
-    int rho;        // residue
-    int64_t lr;     // length of the residue subsequence
-    int64_t q0;     // first query (subsequence index) of the tile
+    int b;      // batch index
+    int rho;    // residue
+    int lr;     // length of the residue subsequence
+    int q0;     // first query (subsequence index) of the tile
 };
 
-__device__ __forceinline__ bool tile_of(const BandGeom& g, Tile& t) {
-    t.b = blockIdx.z;
-    t.rho = blockIdx.y;
-    t.lr = (g.l - t.rho + g.dil - 1) / g.dil;
-    t.q0 = (int64_t)blockIdx.x * kT;
+// Tiles are numbered (tile, residue, batch) with the tile fastest.  Workgroup ids are
+// dealt round-robin to the 8 XCDs; remap them so each XCD owns a contiguous run of
+// tiles of the same sequences, whose key/value blocks then stay in that XCD's L2.
+__device__ __forceinline__ bool tile_of(const BandGeom& g, int ntx, Tile& t) {
+    const int nblk = gridDim.x;
+    const int bid = blockIdx.x;
+    const int id = (nblk & 7) == 0 ? (bid & 7) * (nblk >> 3) + (bid >> 3) : bid;
+    t.q0 = (id % ntx) * kT;
+    const int r = id / ntx;
+    t.rho = r % g.dil;
+    t.b = r / g.dil;
+    t.lr = ((int)g.l - t.rho + g.dil - 1) / g.dil;
     return t.q0 < t.lr;
 }
 
-// Global row (in [b][l]) of subsequence index tq.
-__device__ __forceinline__ int64_t grow(const BandGeom& g, const Tile& t, int64_t tq) {
-    return t.b * g.l + tq * g.dil + t.rho;
+// Row (in [b][l]) of element tq of the tile's subsequence, and its element offset in a
+// [b][l][64] tensor.
+__device__ __forceinline__ int64_t row_index(const BandGeom& g, const Tile& t, int tq) {
+    return (int64_t)t.b * g.l + (int64_t)tq * g.dil + t.rho;
+}
+__device__ __forceinline__ int64_t row_off(const BandGeom& g, const Tile& t, int tq) {
+    return row_index(g, t, tq) * kD;
 }
 
 __device__ __forceinline__ int kswz(int row, int ch) { return row * 8 + (ch ^ (row & 7)); }
 
-// Cooperative load of 64 key rows [t0, t0+64) into LDS (16-byte chunks, XOR swizzle);
-// rows outside [0, lr) are zero.
-__device__ __forceinline__ void load_k_block(const BandGeom& g, const Tile& t,
-                                             const bf16_t* __restrict__ K, int64_t t0,
-                                             u32x4* lk) {
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-        int idx = threadIdx.x + e * 256;
-        int row = idx >> 3, ch = idx & 7;
-        int64_t tt = t0 + row;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (tt >= 0 && tt < t.lr)
-            v = *reinterpret_cast<const u32x4*>(K + grow(g, t, tt) * kD + ch * 8);
-        lk[kswz(row, ch)] = v;
-    }
-}
+// Register staging of one 64-row block of K (and V): 2 x 16 bytes per thread each.
+struct KVRegs {
+    u32x4 k[2];
+    u32x4 v[2];
+};
 
-// Cooperative load of 64 value rows into LDS, transposed: vt[e][t].
-__device__ __forceinline__ void load_vt_block(const BandGeom& g, const Tile& t,
-                                              const bf16_t* __restrict__ V, int64_t t0,
-                                              bf16_t* vt) {
+template <bool WITH_K, bool WITH_V>
+__device__ __forceinline__ void gload_block(const BandGeom& g, const Tile& t,
+                                            const bf16_t* __restrict__ K,
+                                            const bf16_t* __restrict__ V, int t0, KVRegs& r) {
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-        int idx = threadIdx.x + e * 256;
-        int row = idx >> 3, ch = idx & 7;
-        int64_t tt = t0 + row;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (tt >= 0 && tt < t.lr)
-            v = *reinterpret_cast<const u32x4*>(V + grow(g, t, tt) * kD + ch * 8);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            vt[(ch * 8 + 2 * i) * kVtLd + row] = (bf16_t)(v[i] & 0xffffu);
-            vt[(ch * 8 + 2 * i + 1) * kVtLd + row] = (bf16_t)(v[i] >> 16);
+        const int idx = threadIdx.x + e * 256;
+        const int row = idx >> 3, ch = idx & 7;
+        const int tt = t0 + row;
+        u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+        if (tt >= 0 && tt < t.lr) {
+            const int64_t off = row_off(g, t, tt) + ch * 8;
+            if (WITH_K) kv = *reinterpret_cast<const u32x4*>(K + off);
+            if (WITH_V) vv = *reinterpret_cast<const u32x4*>(V + off);
         }
+        r.k[e] = kv;
+        r.v[e] = vv;
     }
 }
 
-// The wave's two Q fragments (d halves) for query q (zero outside [0, lr)).
+// K block: 16-byte chunks with an XOR swizzle (conflict-free ds_read_b128 fragments).
+// V block: plain rows padded to kVLd elements (read through the transposing load).
+template <bool WITH_K, bool WITH_V>
+__device__ __forceinline__ void lstore_block(const KVRegs& r, u32x4* lk, bf16_t* lv) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const int idx = threadIdx.x + e * 256;
+        const int row = idx >> 3, ch = idx & 7;
+        if (WITH_K) lk[kswz(row, ch)] = r.k[e];
+        if (WITH_V) *reinterpret_cast<u32x4*>(lv + row * kVLd + ch * 8) = r.v[e];
+    }
+}
+
+// The lane's two Q fragments (d halves) for query q (zero outside [0, lr)).
 __device__ __forceinline__ void load_q_frags(const BandGeom& g, const Tile& t,
-                                             const bf16_t* __restrict__ Q, int64_t q,
+                                             const bf16_t* __restrict__ Q, int q,
                                              bf16x8 qf[2]) {
     const int grp = (threadIdx.x & 63) >> 4;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
         u32x4 v = {0u, 0u, 0u, 0u};
-        if (q < t.lr) v = *reinterpret_cast<const u32x4*>(Q + grow(g, t, q) * kD + kk * 32 + grp * 8);
+        if (q < t.lr)
+            v = *reinterpret_cast<const u32x4*>(Q + row_off(g, t, q) + kk * 32 + grp * 8);
         qf[kk] = __builtin_bit_cast(bf16x8, v);
     }
 }
 
-// s[ft] = S^T block for keys 16*ft + 4*grp + v of the LDS block and the lane's query.
+// s[ft][v] = K[16*ft + 4*grp + v] . Q[query of the lane] over the LDS key block.
 __device__ __forceinline__ void score_block(const u32x4* lk, const bf16x8 qf[2], f32x4 s[4]) {
     const int lane = threadIdx.x & 63;
     const int grp = lane >> 4;
@@ -118,50 +137,64 @@ __device__ __forceinline__ void score_block(const u32x4* lk, const bf16x8 qf[2],
     }
 }
 
-// o[eb] += V^T[16*eb + l%16][keys] * P^T[keys][query]; p holds the lane's 16 probabilities
-// (p[ft][v] for key 16*ft + 4*grp + v).
-__device__ __forceinline__ void pv_block(const bf16_t* vt, const f32x4 p[4], f32x4 o[4]) {
+__device__ __forceinline__ s16x4 tr_read(const bf16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(p));
+}
+
+// o[eb] (rows e = 16*eb + 4*grp + v, column = the lane's query) += V^T * P^T over the
+// block's 64 keys; p[ft][v] is the lane's probability for key 16*ft + 4*grp + v.
+__device__ __forceinline__ void pv_block(const bf16_t* lv, const f32x4 p[4], f32x4 o[4]) {
     const int lane = threadIdx.x & 63;
     const int grp = lane >> 4;
+    const int li = lane & 15;
+    const int col = 4 * (li & 3);      // this lane addresses a 4-column slice ...
+    const int krow = li >> 2;          // ... of key row 32h + 4*grp + krow (+16)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        bf16_t pb[8];
+        bf16x8 pf;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            pb[v] = f2bf(p[2 * h][v]);
-            pb[4 + v] = f2bf(p[2 * h + 1][v]);
+            pf[v] = (__bf16)p[2 * h][v];
+            pf[4 + v] = (__bf16)p[2 * h + 1][v];
         }
-        bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
+        const bf16_t* base = lv + (32 * h + 4 * grp + krow) * kVLd + col;
 #pragma unroll
         for (int eb = 0; eb < 4; ++eb) {
-            const bf16_t* row = vt + (eb * 16 + (lane & 15)) * kVtLd + h * 32 + 4 * grp;
-            uint2 lo = *reinterpret_cast<const uint2*>(row);
-            uint2 hi = *reinterpret_cast<const uint2*>(row + 16);
-            u32x4 u = {lo.x, lo.y, hi.x, hi.y};
-            o[eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, u), pf,
-                                                            o[eb], 0, 0, 0);
+            s16x4 lo = tr_read(base + eb * 16);
+            s16x4 hi = tr_read(base + 16 * kVLd + eb * 16);
+            s16x4 both[2] = {lo, hi};
+            bf16x8 vf = __builtin_bit_cast(bf16x8, both);
+            o[eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[eb], 0, 0, 0);
         }
     }
 }
 
+__device__ __forceinline__ int n_key_blocks(const BandGeom& g) {
+    return (kT + 2 * (int)g.w + kT - 1) / kT;
+}
+
 // --------------------------------------------------------------------- G2BMM
-__global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, const bf16_t* __restrict__ Q,
+__global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
+                                                        const bf16_t* __restrict__ Q,
                                                         const bf16_t* __restrict__ K,
                                                         float* __restrict__ S) {
     __shared__ u32x4 lk[kT * 8];
     Tile t;
-    if (!tile_of(g, t)) return;
+    if (!tile_of(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
-    const int64_t q = t.q0 + wv * 16 + (lane & 15);
-    const int64_t nb = 2 * g.w + 1;
+    const int q = t.q0 + wv * 16 + (lane & 15);
+    const int w = (int)g.w, nb = 2 * w + 1;
     bf16x8 qf[2];
     load_q_frags(g, t, Q, q, qf);
-    const int nblk = (int)((kT + 2 * g.w + kT - 1) / kT);
-    float* srow = S + (q < t.lr ? grow(g, t, q) : 0) * nb;
+    const int nblk = n_key_blocks(g);
+    float* srow = S + (q < t.lr ? row_index(g, t, q) : 0) * nb;
+    KVRegs r;
     for (int kb = 0; kb < nblk; ++kb) {
-        const int64_t t0 = t.q0 - g.w + (int64_t)kb * kT;
+        const int t0 = t.q0 - w + kb * kT;
+        gload_block<true, false>(g, t, K, nullptr, t0, r);
         __syncthreads();
-        load_k_block(g, t, K, t0, lk);
+        lstore_block<true, false>(r, lk, nullptr);
         __syncthreads();
         f32x4 s[4];
         score_block(lk, qf, s);
@@ -170,7 +203,7 @@ __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, const bf16_
         for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                int64_t j = t0 + ft * 16 + 4 * grp + v - q + g.w;
+                const int j = t0 + ft * 16 + 4 * grp + v - q + w;
                 if (j >= 0 && j < nb) srow[j] = g.scale * s[ft][v];
             }
     }
@@ -184,21 +217,21 @@ __global__ __launch_bounds__(256) void band_softmax_kernel(BandGeom g, const flo
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= g.b * g.l) return;
-    const int64_t i = row % g.l;
-    const int nb = (int)(2 * g.w + 1);
+    const int i = (int)(row % g.l);
+    const int w = (int)g.w, nb = 2 * w + 1, L = (int)g.l;
     const float* s = S + row * nb;
     bf16_t* p = P + row * nb;
     float x[NCH];
     float m = -INFINITY;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        int j = lane + c * 64;
+        const int j = lane + c * 64;
         float val = -INFINITY;
         if (j < nb) {
             val = s[j];
             if (mask) {
-                int64_t tt = i + (int64_t)(j - g.w) * g.dil;
-                if (tt < 0 || tt >= g.l) val = -INFINITY;
+                const int64_t tt = (int64_t)i + (int64_t)(j - w) * g.dil;
+                if (tt < 0 || tt >= L) val = -INFINITY;
             }
         }
         x[c] = val;
@@ -206,10 +239,11 @@ __global__ __launch_bounds__(256) void band_softmax_kernel(BandGeom g, const flo
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    const float ml2 = m * 1.4426950408889634f;
     float sum = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        x[c] = __expf(x[c] - m);
+        x[c] = __builtin_amdgcn_exp2f(x[c] * 1.4426950408889634f - ml2);
         sum += x[c];
     }
 #pragma unroll
@@ -217,130 +251,175 @@ __global__ __launch_bounds__(256) void band_softmax_kernel(BandGeom g, const flo
     const float inv = 1.f / sum;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        int j = lane + c * 64;
+        const int j = lane + c * 64;
         if (j < nb) p[j] = f2bf(x[c] * inv);
     }
 }
 
 // ---------------------------------------------------------------------- GBMM
 template <typename OT>
-__global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, const bf16_t* __restrict__ P,
+__global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
+                                                       const bf16_t* __restrict__ P,
                                                        const bf16_t* __restrict__ V,
                                                        OT* __restrict__ O) {
-    __shared__ bf16_t vt[kD * kVtLd];
+    __shared__ __attribute__((aligned(16))) bf16_t lv[kT * kVLd];
     Tile t;
-    if (!tile_of(g, t)) return;
+    if (!tile_of(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
-    const int64_t q = t.q0 + wv * 16 + (lane & 15);
-    const int64_t nb = 2 * g.w + 1;
-    const bf16_t* prow = P + (q < t.lr ? grow(g, t, q) : 0) * nb;
-    const int nblk = (int)((kT + 2 * g.w + kT - 1) / kT);
+    const int q = t.q0 + wv * 16 + (lane & 15);
+    const int w = (int)g.w, nb = 2 * w + 1;
+    const bf16_t* prow = P + (q < t.lr ? row_index(g, t, q) : 0) * nb;
+    const int nblk = n_key_blocks(g);
     f32x4 o[4];
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    KVRegs r;
     for (int kb = 0; kb < nblk; ++kb) {
-        const int64_t t0 = t.q0 - g.w + (int64_t)kb * kT;
+        const int t0 = t.q0 - w + kb * kT;
+        gload_block<false, true>(g, t, nullptr, V, t0, r);
         __syncthreads();
-        load_vt_block(g, t, V, t0, vt);
+        lstore_block<false, true>(r, nullptr, lv);
         __syncthreads();
         f32x4 p[4];
 #pragma unroll
         for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                int64_t j = t0 + ft * 16 + 4 * grp + v - q + g.w;
+                const int j = t0 + ft * 16 + 4 * grp + v - q + w;
                 p[ft][v] = (q < t.lr && j >= 0 && j < nb) ? bf2f(prow[j]) : 0.f;
             }
-        pv_block(vt, p, o);
+        pv_block(lv, p, o);
     }
     if (q >= t.lr) return;
-    OT* orow = O + grow(g, t, q) * kD;
+    OT* orow = O + row_off(g, t, q);
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) Out<OT>::put4(orow + eb * 16 + 4 * grp, o[eb]);
 }
 
 // --------------------------------------------------------------------- fused
-// G2BMM -> online softmax -> GBMM in one pass over the key blocks of the band;
-// scores and probabilities stay in registers.
-template <typename OT>
-__global__ __launch_bounds__(256) void band_fused_kernel(BandGeom g, const bf16_t* __restrict__ Q,
+// G2BMM -> online softmax -> GBMM in one pass over the key blocks of the band; scores
+// and probabilities stay in registers, K/V blocks are double-buffered in LDS (the next
+// block's global loads are in flight while the current one is computed).
+//
+// Softmax bookkeeping per query (log2 units, x = scale*log2(e)*score): a running
+// reference m and this lane's share l of sum(exp2(x - m)); O accumulates unnormalised.
+// m is raised only when a block's maximum exceeds it by more than kLazy, so most
+// blocks need no rescaling of O; every exp2 argument stays <= kLazy.
+template <typename OT, bool MASK>
+__global__ __launch_bounds__(256) void band_fused_kernel(BandGeom g, int ntx,
+                                                        const bf16_t* __restrict__ Q,
                                                         const bf16_t* __restrict__ K,
                                                         const bf16_t* __restrict__ V,
-                                                        OT* __restrict__ O, int mask) {
-    __shared__ u32x4 lk[kT * 8];
-    __shared__ bf16_t vt[kD * kVtLd];
+                                                        OT* __restrict__ O) {
+    constexpr float kLazy = 8.f;
+    __shared__ u32x4 lk[2][kT * 8];
+    __shared__ __attribute__((aligned(16))) bf16_t lv[2][kT * kVLd];
     Tile t;
-    if (!tile_of(g, t)) return;
+    if (!tile_of(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
-    const int64_t q = t.q0 + wv * 16 + (lane & 15);
-    const float sl2 = g.scale * 1.4426950408889634f;   // scale * log2(e)
+    const int w = (int)g.w;
+    const int qa = t.q0 + wv * 16;        // the wave's first query
+    const int q = qa + (lane & 15);
+    const float sl2 = g.scale * 1.4426950408889634f;
     bf16x8 qf[2];
     load_q_frags(g, t, Q, q, qf);
-    const int nblk = (int)((kT + 2 * g.w + kT - 1) / kT);
+    const int nblk = n_key_blocks(g);
+
     f32x4 o[4];
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY;   // running max of the query's scores (log2 units)
-    float l_run = 0.f;         // this lane's share of the running denominator
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+
+    KVRegs r;
+    gload_block<true, true>(g, t, K, V, t.q0 - w, r);
+    lstore_block<true, true>(r, lk[0], lv[0]);
+    __syncthreads();
     for (int kb = 0; kb < nblk; ++kb) {
-        const int64_t t0 = t.q0 - g.w + (int64_t)kb * kT;
-        __syncthreads();
-        load_k_block(g, t, K, t0, lk);
-        load_vt_block(g, t, V, t0, vt);
-        __syncthreads();
-        f32x4 s[4];
-        score_block(lk, qf, s);
-        float mb = -INFINITY;
+        const int cur = kb & 1;
+        const int t0 = t.q0 - w + kb * kT;
+        if (kb + 1 < nblk) gload_block<true, true>(g, t, K, V, t0 + kT, r);
+        // does the block meet the wave's band at all, and is it entirely inside it?
+        const bool any = t0 + kT - 1 >= qa - w && t0 <= qa + 15 + w;
+        if (any) {
+            bool full = t0 - (qa + 15) >= -w && t0 + kT - 1 - qa <= w;
+            if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
+            f32x4 s[4];
+            score_block(lk[cur], qf, s);
+            float mb = -INFINITY;
+            if (full) {
 #pragma unroll
-        for (int ft = 0; ft < 4; ++ft)
+                for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                int64_t tt = t0 + ft * 16 + 4 * grp + v;
-                int64_t dj = tt - q;   // j - w
-                bool live = dj >= -g.w && dj <= g.w && (!mask || (tt >= 0 && tt < t.lr));
-                float x = live ? s[ft][v] * sl2 : -INFINITY;
-                s[ft][v] = x;
-                mb = fmaxf(mb, x);
+                    for (int v = 0; v < 4; ++v) {
+                        s[ft][v] *= sl2;
+                        mb = fmaxf(mb, s[ft][v]);
+                    }
+            } else {
+#pragma unroll
+                for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int tt = t0 + ft * 16 + 4 * grp + v;
+                        const int dj = tt - q;
+                        bool live = dj >= -w && dj <= w;
+                        if (MASK) live = live && tt >= 0 && tt < t.lr;
+                        const float x = live ? s[ft][v] * sl2 : -INFINITY;
+                        s[ft][v] = x;
+                        mb = fmaxf(mb, x);
+                    }
             }
-        mb = fmaxf(mb, __shfl_xor(mb, 16));
-        mb = fmaxf(mb, __shfl_xor(mb, 32));
-        const float m_new = fmaxf(m_run, mb);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float corr = exp2f(m_run - m_use);
-        m_run = m_new;
-        float ls = 0.f;
+            mb = fmaxf(mb, __shfl_xor(mb, 16));
+            mb = fmaxf(mb, __shfl_xor(mb, 32));
+            const bool need = mb > m_run + kLazy;
+            if (__any(need)) {
+                const float m_new = need ? mb : m_run;
+                const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= corr;
 #pragma unroll
-        for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                float pv = exp2f(s[ft][v] - m_use);
-                s[ft][v] = pv;
-                ls += pv;
+                for (int eb = 0; eb < 4; ++eb) o[eb] *= corr;
+                m_run = m_new;
             }
-        l_run = l_run * corr + ls;
+            const float m_use = m_run == -INFINITY ? 0.f : m_run;
 #pragma unroll
-        for (int eb = 0; eb < 4; ++eb) o[eb] *= corr;
-        pv_block(vt, s, o);
+            for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float pv = __builtin_amdgcn_exp2f(s[ft][v] - m_use);
+                    s[ft][v] = pv;
+                    l_run += pv;
+                }
+            pv_block(lv[cur], s, o);
+        }
+        if (kb + 1 < nblk) lstore_block<true, true>(r, lk[cur ^ 1], lv[cur ^ 1]);
+        __syncthreads();
     }
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
     if (q >= t.lr) return;
     const float inv = 1.f / l_run;
-    OT* orow = O + grow(g, t, q) * kD;
+    OT* orow = O + row_off(g, t, q);
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) Out<OT>::put4(orow + eb * 16 + 4 * grp, o[eb] * inv);
 }
 
-dim3 tile_grid(const BandGeom& g) {
-    int64_t l0 = (g.l + g.dil - 1) / g.dil;   // longest residue subsequence (rho = 0)
-    return dim3((unsigned)((l0 + kT - 1) / kT), (unsigned)g.dil, (unsigned)g.b);
+struct Grid {
+    dim3 grid;
+    int ntx;
+};
+
+Grid tile_grid(const BandGeom& g) {
+    const int64_t l0 = (g.l + g.dil - 1) / g.dil;   // longest residue subsequence (rho = 0)
+    const int ntx = (int)((l0 + kT - 1) / kT);
+    return {dim3((unsigned)(ntx * g.dil * g.b)), ntx};
 }
 
 }  // namespace
 
 hipError_t launch_band_g2bmm(const BandGeom& g, const void* q, const void* k, float* s,
                              hipStream_t stream) {
-    hipLaunchKernelGGL(band_g2bmm_kernel, tile_grid(g), dim3(256), 0, stream, g,
+    Grid gr = tile_grid(g);
+    hipLaunchKernelGGL(band_g2bmm_kernel, gr.grid, dim3(256), 0, stream, g, gr.ntx,
                        (const bf16_t*)q, (const bf16_t*)k, s);
     return hipGetLastError();
 }
@@ -365,25 +444,30 @@ hipError_t launch_band_softmax(const BandGeom& g, const float* s, void* p, int m
 
 hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, void* o,
                             int o_bf16, hipStream_t stream) {
+    Grid gr = tile_grid(g);
     if (o_bf16)
-        hipLaunchKernelGGL(band_gbmm_kernel<bf16_t>, tile_grid(g), dim3(256), 0, stream, g,
+        hipLaunchKernelGGL(band_gbmm_kernel<bf16_t>, gr.grid, dim3(256), 0, stream, g, gr.ntx,
                            (const bf16_t*)p, (const bf16_t*)v, (bf16_t*)o);
     else
-        hipLaunchKernelGGL(band_gbmm_kernel<float>, tile_grid(g), dim3(256), 0, stream, g,
+        hipLaunchKernelGGL(band_gbmm_kernel<float>, gr.grid, dim3(256), 0, stream, g, gr.ntx,
                            (const bf16_t*)p, (const bf16_t*)v, (float*)o);
     return hipGetLastError();
 }
 
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
                              void* o, int o_bf16, int mask, hipStream_t stream) {
-    if (o_bf16)
-        hipLaunchKernelGGL(band_fused_kernel<bf16_t>, tile_grid(g), dim3(256), 0, stream, g,
-                           (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (bf16_t*)o,
-                           mask);
-    else
-        hipLaunchKernelGGL(band_fused_kernel<float>, tile_grid(g), dim3(256), 0, stream, g,
-                           (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (float*)o,
-                           mask);
+    Grid gr = tile_grid(g);
+#define OLLIE_FUSED(OT, M)                                                                    \
+    hipLaunchKernelGGL((band_fused_kernel<OT, M>), gr.grid, dim3(256), 0, stream, g, gr.ntx, \
+                       (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
+    if (o_bf16) {
+        if (mask) OLLIE_FUSED(bf16_t, true);
+        else OLLIE_FUSED(bf16_t, false);
+    } else {
+        if (mask) OLLIE_FUSED(float, true);
+        else OLLIE_FUSED(float, false);
+    }
+#undef OLLIE_FUSED
     return hipGetLastError();
 }
 
