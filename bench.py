@@ -15,6 +15,9 @@ on.  `roofline` covers the kernel that takes the largest share of a step.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workloads.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+       python bench.py --stage NAME [--steps K]   (launch one stage kernel K times, for
+       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg> for cfg 2-4, or band_fused,
+       band_g2bmm, band_softmax, band_gbmm)
 """
 from __future__ import annotations
 
@@ -68,6 +71,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--stage", default=None, help="launch only this stage kernel")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this library has no multi-GPU path "
@@ -113,6 +117,10 @@ def main():
     def band_call():
         ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale, mask_invalid=bwl.mask_invalid,
                       out=o)
+
+    if args.stage:
+        run_stage(args, conv_ops, bwl, q, k, v, o, stream)
+        return
 
     def step(evs=None):
         for i, op in enumerate(conv_ops):
@@ -214,6 +222,53 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
+    """Launch one stage kernel `steps` times after `warmup` launches; print its
+    HIP-event average (for rocprofv3 runs that should see a single kernel/workload)."""
+    import torch
+    import paper_2208_02025_amd as ol
+
+    name = args.stage
+    fn = None
+    if ":" in name:
+        kind, cfg = name.split(":")
+        op = next(o_ for o_ in conv_ops if o_["cfg"] == int(cfg))
+        y = op["ws"][:op["m"] * op["nc"] * 4].view(torch.float32).view(op["m"], op["nc"])
+        a = op["x"].view(op["m"], op["wl"].c)
+        b = op["wt"].view(op["nc"], op["wl"].c)
+        if kind == "gemm":
+            fn = lambda: ol.gemm_nt(a, b, out=y)
+        elif kind == "eop":
+            ol.gemm_nt(a, b, out=y)
+            fn = lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y, out=op["out"])
+        elif kind == "op":
+            fn = lambda: op["entry"](op["x"], op["wt"], **op["kw"])
+    elif name == "band_fused":
+        fn = lambda: ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale,
+                                   mask_invalid=bwl.mask_invalid, out=o)
+    elif name in ("band_g2bmm", "band_softmax", "band_gbmm"):
+        s = ol.band_g2bmm(q, k, bwl.w, bwl.dilation, bwl.scale)
+        p = ol.band_softmax(s, bwl.w, bwl.dilation, bwl.mask_invalid)
+        fn = {"band_g2bmm": lambda: ol.band_g2bmm(q, k, bwl.w, bwl.dilation, bwl.scale, s=s),
+              "band_softmax": lambda: ol.band_softmax(s, bwl.w, bwl.dilation,
+                                                      bwl.mask_invalid, p=p),
+              "band_gbmm": lambda: ol.band_gbmm(p, v, bwl.w, bwl.dilation, o=o)}[name]
+    if fn is None:
+        raise SystemExit(f"unknown stage {name}")
+    for _ in range(args.warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        fn()
+    e1.record(stream)
+    e1.synchronize()
+    print(json.dumps({"stage": name, "launches": args.steps,
+                      "avg_ms": round(e0.elapsed_time(e1) / args.steps, 5)}), flush=True)
 
 
 def cpu_baseline(conv_ops, bwl):
