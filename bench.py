@@ -16,8 +16,8 @@ on.  `roofline` covers the kernel that takes the largest share of a step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
        python bench.py --stage NAME [--steps K]   (launch one stage kernel K times, for
-       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg> for cfg 2-4, or band_fused,
-       band_g2bmm, band_softmax, band_gbmm)
+       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg> for cfg 2-4, band_fused,
+       band_g2bmm, band_softmax, band_gbmm, or copy = a plain 256 MiB device copy)
 """
 from __future__ import annotations
 
@@ -255,6 +255,11 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
               "band_softmax": lambda: ol.band_softmax(s, bwl.w, bwl.dilation,
                                                       bwl.mask_invalid, p=p),
               "band_gbmm": lambda: ol.band_gbmm(p, v, bwl.w, bwl.dilation, o=o)}[name]
+    elif name == "copy":
+        # plain device copy of 256 MiB: the reference for scaling HBM traffic counters
+        src = torch.empty(64 << 20, dtype=torch.float32, device=q.device).fill_(1.0)
+        dst = torch.empty_like(src)
+        fn = lambda: dst.copy_(src)
     if fn is None:
         raise SystemExit(f"unknown stage {name}")
     for _ in range(args.warmup):

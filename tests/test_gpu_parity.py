@@ -181,7 +181,12 @@ def test_small_shapes_bf16(ci, integer):
 
 # ----------------------------------------------------------------- stage entry points
 
-@pytest.mark.parametrize("m,n,k", [(1, 1, 8), (129, 257, 72), (300, 130, 200), (64, 64, 64)])
+# k % 64 != 0 takes the register-staged kernel; k % 64 == 0 the DMA kernel, whose tile
+# configuration follows the shape: (4129, 4136) -> 256x128/3 stages, (2100, 2100) ->
+# 128x128/2 stages, the others -> 128x128/3 stages (all with ragged m and n tails).
+@pytest.mark.parametrize("m,n,k", [(1, 1, 8), (129, 257, 72), (300, 130, 200), (64, 64, 64),
+                                   (200, 300, 128), (300, 130, 192), (2100, 2100, 64),
+                                   (4129, 4136, 128)])
 def test_gemm_stage_bf16_integer_exact(m, n, k):
     say("gemm bf16", m, n, k)
     a = synth.random_tensor((m, k), 6000 + m, "bf16", integer=True)
