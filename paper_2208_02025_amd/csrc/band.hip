@@ -22,6 +22,8 @@
 // each 16-lane group receives element i%4 of the 8-byte rows addressed by lanes
 // i/4 + 4j (j = 0..3): lanes address rows (keys) and 4-column slices, the hardware
 // returns one column (value dimension) across four keys.
+#include <stdlib.h>
+
 #include "common.h"
 
 namespace ollie {
@@ -301,106 +303,216 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
 // and probabilities stay in registers, K/V blocks are double-buffered in LDS (the next
 // block's global loads are in flight while the current one is computed).
 //
-// Softmax bookkeeping per query (log2 units, x = scale*log2(e)*score): a running
-// reference m and this lane's share l of sum(exp2(x - m)); O accumulates unnormalised.
-// m is raised only when a block's maximum exceeds it by more than kLazy, so most
-// blocks need no rescaling of O; every exp2 argument stays <= kLazy.
-template <typename OT, bool MASK>
-__global__ __launch_bounds__(256) void band_fused_kernel(BandGeom g, int ntx,
+// Each wave owns QH 16-query groups; with QH = 2 every K and V fragment read from LDS
+// feeds two MFMAs (at the cost of occupancy).  Softmax bookkeeping per query, in log2 units
+// (x = scale*log2(e)*score): a running reference m, and the denominator and O both
+// accumulated unnormalised by MFMA -- the denominator as the product of an all-ones
+// operand with the same bf16 probabilities that multiply V, so O and its normaliser
+// see identical rounding.  m is raised only when a block's maximum exceeds it by more
+// than kLazy, so most blocks need no rescaling and every exp2 argument stays <= kLazy.
+// The scale enters as one FMA per score; a negative scale is handled by negating the
+// query fragments (an exact sign flip of bf16) and using |scale|.
+template <typename OT, bool MASK, int QH>
+__global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGeom g, int ntx,
                                                         const bf16_t* __restrict__ Q,
                                                         const bf16_t* __restrict__ K,
                                                         const bf16_t* __restrict__ V,
                                                         OT* __restrict__ O) {
     constexpr float kLazy = 8.f;
+    constexpr int kQPW = 16 * QH;        // queries per wave
+    constexpr int kFT = kQPW * 4;        // queries per tile (4 waves)
     __shared__ u32x4 lk[2][kT * 8];
     __shared__ __attribute__((aligned(16))) bf16_t lv[2][kT * kVLd];
+    // tile geometry (kFT queries per tile)
     Tile t;
-    if (!tile_of(g, ntx, t)) return;
+    {
+        const int nblk_all = gridDim.x;
+        const int bid = blockIdx.x;
+        const int id = (nblk_all & 7) == 0 ? (bid & 7) * (nblk_all >> 3) + (bid >> 3) : bid;
+        t.q0 = (id % ntx) * kFT;
+        const int r = id / ntx;
+        t.rho = r % g.dil;
+        t.b = r / g.dil;
+        t.lr = ((int)g.l - t.rho + g.dil - 1) / g.dil;
+        if (t.q0 >= t.lr) return;
+    }
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
     const int w = (int)g.w;
-    const int qa = t.q0 + wv * 16;        // the wave's first query
-    const int q = qa + (lane & 15);
-    const float sl2 = g.scale * 1.4426950408889634f;
-    bf16x8 qf[2];
-    load_q_frags(g, t, Q, q, qf);
-    const int nblk = n_key_blocks(g);
+    const int qa = t.q0 + wv * kQPW;      // the wave's first query
+    const float sl2 = fabsf(g.scale) * 1.4426950408889634f;
+    const uint32_t qflip = g.scale < 0.f ? 0x80008000u : 0u;
 
-    f32x4 o[4];
+    bf16x8 qf[QH][2];
 #pragma unroll
-    for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY;
-    float l_run = 0.f;
+    for (int hq = 0; hq < QH; ++hq) {
+        const int q = qa + hq * 16 + (lane & 15);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (q < t.lr)
+                v = *reinterpret_cast<const u32x4*>(Q + row_off(g, t, q) + kk * 32 + grp * 8);
+            v ^= (u32x4){qflip, qflip, qflip, qflip};
+            qf[hq][kk] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    const int span = kFT + 2 * w;
+    const int nblk = (span + kT - 1) / kT;
 
+    f32x4 o[QH][4], lsum[QH];
+#pragma unroll
+    for (int hq = 0; hq < QH; ++hq) {
+        lsum[hq] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb) o[hq][eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+    float m_run[QH];
+#pragma unroll
+    for (int hq = 0; hq < QH; ++hq) m_run[hq] = -INFINITY;
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, (u32x4){0x3f803f80u, 0x3f803f80u,
+                                                          0x3f803f80u, 0x3f803f80u});
+
+    // this thread's two 16-byte chunks of every K/V block: rows r0 and r0 + 32
+    const int r0 = threadIdx.x >> 3, ch = threadIdx.x & 7;
+    const int64_t row_step = (int64_t)kT * g.dil * kD;          // 64 subsequence rows
+    const int64_t half_step = (int64_t)32 * g.dil * kD;
+    int tt0 = t.q0 - w + r0;                                     // subsequence row of chunk 0
+    int64_t off0 = ((int64_t)t.b * g.l + t.rho) * kD + (int64_t)tt0 * g.dil * kD + ch * 8;
     KVRegs r;
-    gload_block<true, true>(g, t, K, V, t.q0 - w, r);
+    auto gload = [&]() {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int tt = tt0 + 32 * e;
+            u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+            if (tt >= 0 && tt < t.lr) {
+                kv = *reinterpret_cast<const u32x4*>(K + off0 + e * half_step);
+                vv = *reinterpret_cast<const u32x4*>(V + off0 + e * half_step);
+            }
+            r.k[e] = kv;
+            r.v[e] = vv;
+        }
+        tt0 += kT;
+        off0 += row_step;
+    };
+    gload();
     lstore_block<true, true>(r, lk[0], lv[0]);
     __syncthreads();
+
     for (int kb = 0; kb < nblk; ++kb) {
         const int cur = kb & 1;
         const int t0 = t.q0 - w + kb * kT;
-        if (kb + 1 < nblk) gload_block<true, true>(g, t, K, V, t0 + kT, r);
-        // does the block meet the wave's band at all, and is it entirely inside it?
-        const bool any = t0 + kT - 1 >= qa - w && t0 <= qa + 15 + w;
+        if (kb + 1 < nblk) gload();
+        const bool any = t0 + kT - 1 >= qa - w && t0 <= qa + kQPW - 1 + w;
         if (any) {
-            bool full = t0 - (qa + 15) >= -w && t0 + kT - 1 - qa <= w;
-            if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
-            f32x4 s[4];
-            score_block(lk[cur], qf, s);
-            float mb = -INFINITY;
-            if (full) {
+            // per query half: does the block meet its band, and is it entirely inside?
+            f32x4 s[QH][4];
+            const u32x4* lkc = lk[cur];
 #pragma unroll
-                for (int ft = 0; ft < 4; ++ft)
+            for (int ft = 0; ft < 4; ++ft) {
+                const int row = ft * 16 + (lane & 15);
+                const bf16x8 k0 = __builtin_bit_cast(bf16x8, lkc[kswz(row, grp)]);
+                const bf16x8 k1 = __builtin_bit_cast(bf16x8, lkc[kswz(row, 4 + grp)]);
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        s[ft][v] *= sl2;
-                        mb = fmaxf(mb, s[ft][v]);
-                    }
-            } else {
-#pragma unroll
-                for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int tt = t0 + ft * 16 + 4 * grp + v;
-                        const int dj = tt - q;
-                        bool live = dj >= -w && dj <= w;
-                        if (MASK) live = live && tt >= 0 && tt < t.lr;
-                        const float x = live ? s[ft][v] * sl2 : -INFINITY;
-                        s[ft][v] = x;
-                        mb = fmaxf(mb, x);
-                    }
-            }
-            mb = fmaxf(mb, __shfl_xor(mb, 16));
-            mb = fmaxf(mb, __shfl_xor(mb, 32));
-            const bool need = mb > m_run + kLazy;
-            if (__any(need)) {
-                const float m_new = need ? mb : m_run;
-                const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
-                l_run *= corr;
-#pragma unroll
-                for (int eb = 0; eb < 4; ++eb) o[eb] *= corr;
-                m_run = m_new;
-            }
-            const float m_use = m_run == -INFINITY ? 0.f : m_run;
-#pragma unroll
-            for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const float pv = __builtin_amdgcn_exp2f(s[ft][v] - m_use);
-                    s[ft][v] = pv;
-                    l_run += pv;
+                for (int hq = 0; hq < QH; ++hq) {
+                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[hq][0], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[hq][1], acc, 0, 0, 0);
+                    s[hq][ft] = acc;
                 }
-            pv_block(lv[cur], s, o);
+            }
+            bf16x8 pf[QH][2];
+#pragma unroll
+            for (int hq = 0; hq < QH; ++hq) {
+                const int qh = qa + hq * 16;              // first query of this half
+                const int q = qh + (lane & 15);
+                bool full = t0 - (qh + 15) >= -w && t0 + kT - 1 - qh <= w;
+                if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
+                // live(ft, v): key t0+16ft+4grp+v is inside the query's band (and, in mask
+                // mode, inside the sequence)
+                auto live = [&](int ft, int v) {
+                    const int tt = t0 + ft * 16 + 4 * grp + v;
+                    const int dj = tt - q;
+                    bool l = dj >= -w && dj <= w;
+                    if (MASK) l = l && tt >= 0 && tt < t.lr;
+                    return l;
+                };
+                float mb = -INFINITY;
+                if (full) {
+#pragma unroll
+                    for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) mb = fmaxf(mb, s[hq][ft][v]);
+                } else {
+#pragma unroll
+                    for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            if (live(ft, v)) mb = fmaxf(mb, s[hq][ft][v]);
+                }
+                mb = fmaxf(mb, __shfl_xor(mb, 16));
+                mb = fmaxf(mb, __shfl_xor(mb, 32));
+                const float mbx = mb * sl2;               // block max in log2 units
+                const bool need = mbx > m_run[hq] + kLazy;
+                if (__any(need)) {
+                    const float m_new = need ? mbx : m_run[hq];
+                    const float corr = __builtin_amdgcn_exp2f(m_run[hq] - m_new);
+                    lsum[hq] *= corr;
+#pragma unroll
+                    for (int eb = 0; eb < 4; ++eb) o[hq][eb] *= corr;
+                    m_run[hq] = m_new;
+                }
+                const float nm = m_run[hq] == -INFINITY ? 0.f : -m_run[hq];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    bf16x8 pv;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h][v], sl2, nm));
+                        float p1 =
+                            __builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h + 1][v], sl2, nm));
+                        if (!full) {
+                            p0 = live(2 * h, v) ? p0 : 0.f;
+                            p1 = live(2 * h + 1, v) ? p1 : 0.f;
+                        }
+                        pv[v] = (__bf16)p0;
+                        pv[4 + v] = (__bf16)p1;
+                    }
+                    pf[hq][h] = pv;
+                }
+            }
+            // O^T += V^T P^T and the denominator += 1^T P^T, over the block's keys
+            const bf16_t* lvc = lv[cur];
+            const int li = lane & 15;
+            const bf16_t* base = lvc + (4 * grp + (li >> 2)) * kVLd + 4 * (li & 3);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                for (int eb = 0; eb < 4; ++eb) {
+                    const bf16_t* p = base + 32 * h * kVLd + eb * 16;
+                    s16x4 both[2] = {tr_read(p), tr_read(p + 16 * kVLd)};
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, both);
+#pragma unroll
+                    for (int hq = 0; hq < QH; ++hq)
+                        o[hq][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[hq][h],
+                                                                            o[hq][eb], 0, 0, 0);
+                }
+#pragma unroll
+                for (int hq = 0; hq < QH; ++hq)
+                    lsum[hq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[hq][h],
+                                                                       lsum[hq], 0, 0, 0);
+            }
         }
         if (kb + 1 < nblk) lstore_block<true, true>(r, lk[cur ^ 1], lv[cur ^ 1]);
         __syncthreads();
     }
-    l_run += __shfl_xor(l_run, 16);
-    l_run += __shfl_xor(l_run, 32);
-    if (q >= t.lr) return;
-    const float inv = 1.f / l_run;
-    OT* orow = O + row_off(g, t, q);
 #pragma unroll
-    for (int eb = 0; eb < 4; ++eb) Out<OT>::put4(orow + eb * 16 + 4 * grp, o[eb] * inv);
+    for (int hq = 0; hq < QH; ++hq) {
+        const int q = qa + hq * 16 + (lane & 15);
+        if (q >= t.lr) continue;
+        const float inv = 1.f / lsum[hq][0];
+        OT* orow = O + row_off(g, t, q);
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb) Out<OT>::put4(orow + eb * 16 + 4 * grp, o[hq][eb] * inv);
+    }
 }
 
 struct Grid {
@@ -456,17 +568,28 @@ hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, voi
 
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
                              void* o, int o_bf16, int mask, hipStream_t stream) {
-    Grid gr = tile_grid(g);
-#define OLLIE_FUSED(OT, M)                                                                    \
-    hipLaunchKernelGGL((band_fused_kernel<OT, M>), gr.grid, dim3(256), 0, stream, g, gr.ntx, \
+    // OLLIE_BAND_QH (1 or 2) overrides the queries-per-wave choice, for tuning sweeps
+    static const int qh_env = [] {
+        const char* e = getenv("OLLIE_BAND_QH");
+        return e ? atoi(e) : 0;
+    }();
+    const int qh = qh_env == 2 ? 2 : 1;
+    const int64_t l0 = (g.l + g.dil - 1) / g.dil;
+    const int ntx = (int)((l0 + 64 * qh - 1) / (64 * qh));
+    const dim3 grid((unsigned)(ntx * g.dil * g.b));
+#define OLLIE_FUSED(OT, M, QH)                                                                \
+    hipLaunchKernelGGL((band_fused_kernel<OT, M, QH>), grid, dim3(256), 0, stream, g, ntx,     \
                        (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
+#define OLLIE_FUSED_QH(OT, M) \
+    do { if (qh == 2) OLLIE_FUSED(OT, M, 2); else OLLIE_FUSED(OT, M, 1); } while (0)
     if (o_bf16) {
-        if (mask) OLLIE_FUSED(bf16_t, true);
-        else OLLIE_FUSED(bf16_t, false);
+        if (mask) OLLIE_FUSED_QH(bf16_t, true);
+        else OLLIE_FUSED_QH(bf16_t, false);
     } else {
-        if (mask) OLLIE_FUSED(float, true);
-        else OLLIE_FUSED(float, false);
+        if (mask) OLLIE_FUSED_QH(float, true);
+        else OLLIE_FUSED_QH(float, false);
     }
+#undef OLLIE_FUSED_QH
 #undef OLLIE_FUSED
     return hipGetLastError();
 }

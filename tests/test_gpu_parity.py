@@ -365,3 +365,16 @@ def test_band_fused_and_staged_agree_at_full_size():
     assert torch.isfinite(o1).all() and torch.isfinite(o2).all()
     d = (o1 - o2).abs().max().item() / o2.abs().max().item()
     assert d <= TOL_BF16
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.3])
+@pytest.mark.parametrize("mask", [False, True])
+@pytest.mark.parametrize("staged", [False, True])
+def test_band_scale_edge_cases(scale, mask, staged):
+    """Zero scale (uniform softmax over the live entries) and a negative scale."""
+    say("band scale", scale, "mask", mask, "staged", staged)
+    b, l, w, dil = 2, 211, 9, 2
+    q = synth.random_tensor((b, l, 64), 15000, "bf16", dist="normal")
+    k = synth.random_tensor((b, l, 64), 15001, "bf16", dist="normal")
+    v = synth.random_tensor((b, l, 64), 15002, "bf16", dist="normal")
+    check_band(q, k, v, w, dil, scale, mask, staged)
