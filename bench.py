@@ -16,7 +16,7 @@ on.  `roofline` covers the kernel that takes the largest share of a step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
        python bench.py --stage NAME [--steps K]   (launch one stage kernel K times, for
-       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg> for cfg 2-4, band_fused,
+       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg>, fused:<cfg> for cfg 2-4, band_fused,
        band_g2bmm, band_softmax, band_gbmm, or copy = a plain 256 MiB device copy)
 """
 from __future__ import annotations
@@ -245,6 +245,8 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
             fn = lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y, out=op["out"])
         elif kind == "op":
             fn = lambda: op["entry"](op["x"], op["wt"], **op["kw"])
+        elif kind == "fused":
+            fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=True))
     elif name == "band_fused":
         fn = lambda: ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale,
                                    mask_invalid=bwl.mask_invalid, out=o)

@@ -56,6 +56,7 @@ typedef enum {
 } ollie_dtype;
 
 /* flags */
+#define OLLIE_FUSE_EPILOGUE     (1u << 0)  /* conv: fused GEMM + eOperator, no Y (see below)   */
 #define OLLIE_Y_BF16            (1u << 1)  /* conv: hold the GEMM scope Y in bf16 (default fp32) */
 #define OLLIE_BAND_STAGED       (1u << 2)  /* band: three kernels through S and P in the workspace */
 #define OLLIE_BAND_MASK_INVALID (1u << 3)  /* band: keys outside [0,l) are left out of the softmax */
@@ -110,7 +111,8 @@ int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, 
 
 /* Bytes of workspace that derived_conv2d / derived_dilated_conv2d /
  * derived_conv_transpose2d need: the instantiated scope Y [n*h*w][r*s*k] in fp32
- * (or bf16 with OLLIE_Y_BF16).  Returns 0 for invalid geometry. */
+ * (or bf16 with OLLIE_Y_BF16); 0 when OLLIE_FUSE_EPILOGUE is set and the fused kernel
+ * covers the shape.  Returns 0 for invalid geometry. */
 size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags);
 
 /* Bytes of workspace banded_bmm needs: 0 for the fused path; with OLLIE_BAND_STAGED,
@@ -133,8 +135,17 @@ const char* ollie_version(void);
  *   out[n][ho][wo][k] = sum_{r,s} [0 <= hi < h][0 <= wi < w] Y[(n*h+hi)*w+wi][(r*S+s)*K+k]
  *   with hi = ho*stride_h - pad_h + r, wi = wo*stride_w - pad_w + s.
  * x: X, wt: Wt, out: out (layouts above).  ws: workspace of at least
- * ollie_conv_workspace_bytes(desc, 0, flags) bytes (holds Y).  flags: OLLIE_Y_BF16.
- * Rejects dil != 1 (OLLIE_EINVAL; use derived_dilated_conv2d). */
+ * ollie_conv_workspace_bytes(desc, 0, flags) bytes (holds Y).  flags: OLLIE_Y_BF16,
+ * OLLIE_FUSE_EPILOGUE.
+ * Rejects dil != 1 (OLLIE_EINVAL; use derived_dilated_conv2d).
+ *
+ * OLLIE_FUSE_EPILOGUE evaluates the expression obtained by fusing the GEMM scope into
+ * the eOperator (expression fusion, section 4.1): one contraction over (tap, c) per
+ * output element, so Y is never formed and ws may be NULL.  It covers bf16 inputs with
+ * c % 64 == 0, at most 64 taps and, for the transposed operator, at most 16 stride
+ * residue classes; other shapes take the two-stage path, which needs the workspace.
+ * Summation order differs from the two-stage path, so fp32 results agree to rounding
+ * (integer-valued inputs agree exactly). */
 int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                    void* ws, size_t ws_bytes, uint32_t flags, void* stream);
 

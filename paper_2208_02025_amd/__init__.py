@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libollie.so")
 
 OK, EINVAL, EDTYPE, EWORKSPACE, EALIGN, EHIP = range(6)
 F32, BF16 = 0, 1
+FUSE_EPILOGUE = 1 << 0
 Y_BF16 = 1 << 1
 BAND_STAGED = 1 << 2
 BAND_MASK_INVALID = 1 << 3
@@ -160,14 +161,14 @@ def conv_workspace_bytes(desc: ConvDesc, transposed: bool, flags: int = 0) -> in
 
 
 def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output_padding,
-          out_dtype, y_bf16, out, ws):
+          out_dtype, y_bf16, out, ws, fuse=False):
     _gpu(x, "x")
     _gpu(wt, "wt")
     if x.dtype != wt.dtype:
         raise ValueError("x and wt must have the same dtype")
     desc = conv_desc(tuple(x.shape), tuple(wt.shape), stride, padding, dilation, output_padding,
                      x.dtype, out_dtype)
-    flags = Y_BF16 if y_bf16 else 0
+    flags = (Y_BF16 if y_bf16 else 0) | (FUSE_EPILOGUE if fuse else 0)
     ho, wo = conv_out_hw(desc, transposed)
     if out is None:
         out = torch.empty((desc.n, ho, wo, desc.k), dtype=out_dtype, device=x.device)
@@ -176,35 +177,37 @@ def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output
         if tuple(out.shape) != (desc.n, ho, wo, desc.k) or out.dtype != out_dtype:
             raise ValueError("out has the wrong shape or dtype")
     need = conv_workspace_bytes(desc, transposed, flags)
-    if ws is None:
+    if ws is None and need:
         ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     st = getattr(load_library(), entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out),
-                                        _ptr(ws), ws.numel() * ws.element_size(), flags,
-                                        _stream(x.device))
+                                        _ptr(ws), ws_bytes, flags, _stream(x.device))
     _check(st, entry)
     return out
 
 
 def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=False,
-                   out=None, ws=None):
-    """Conv2d (dilation 1) as GEMM + OffsetAdd eOperator.  x [N,H,W,C], wt [R,S,K,C]."""
+                   out=None, ws=None, fuse=False):
+    """Conv2d (dilation 1) as GEMM + OffsetAdd eOperator (fuse=True: the fused
+    expression, no Y).  x [N,H,W,C], wt [R,S,K,C]."""
     return _conv("derived_conv2d", False, x, wt, stride, padding, 1, 0, out_dtype, y_bf16,
-                 out, ws)
+                 out, ws, fuse)
 
 
 def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,
-                           y_bf16=False, out=None, ws=None):
+                           y_bf16=False, out=None, ws=None, fuse=False):
     """Dilated Conv2d as GEMM + dilated OffsetAdd eOperator."""
     return _conv("derived_dilated_conv2d", False, x, wt, stride, padding, dilation, 0,
-                 out_dtype, y_bf16, out, ws)
+                 out_dtype, y_bf16, out, ws, fuse)
 
 
 def derived_conv_transpose2d(x, wt, stride=1, padding=0, output_padding=0, dilation=1,
-                             out_dtype=torch.float32, y_bf16=False, out=None, ws=None):
+                             out_dtype=torch.float32, y_bf16=False, out=None, ws=None,
+                             fuse=False):
     """ConvTranspose2d as GEMM on the unpadded input + selective-add eOperator.
     x [N,H,W,C_in], wt [R,S,C_out,C_in]."""
     return _conv("derived_conv_transpose2d", True, x, wt, stride, padding, dilation,
-                 output_padding, out_dtype, y_bf16, out, ws)
+                 output_padding, out_dtype, y_bf16, out, ws, fuse)
 
 
 def band_desc(q_shape, w, dilation, scale=1.0, out_dtype=torch.float32) -> BandDesc:

@@ -92,7 +92,15 @@ ConvGeom conv_geom(const ollie_conv_desc* d, int64_t ho, int64_t wo) {
     return g;
 }
 
-size_t conv_ws(const ollie_conv_desc* d, uint32_t flags) {
+bool fused_path(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
+                uint32_t flags) {
+    return (flags & OLLIE_FUSE_EPILOGUE) && d->in_dtype == OLLIE_BF16 &&
+           conv_fused_supported(conv_geom(d, ho, wo), transposed);
+}
+
+size_t conv_ws(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
+               uint32_t flags) {
+    if (fused_path(d, transposed, ho, wo, flags)) return 0;
     return (size_t)(d->n * d->h * d->w) * (size_t)(d->r * d->s * d->k) *
            ((flags & OLLIE_Y_BF16) ? 2 : 4);
 }
@@ -118,11 +126,21 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     int64_t ho, wo;
     int st = check_conv_geom(d, transposed, &ho, &wo);
     if (st) return st;
-    if (flags & ~(uint32_t)OLLIE_Y_BF16) return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
-    if (!x || !wt || !out || !ws) return fail(OLLIE_EINVAL, "null tensor or workspace pointer");
+    if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE))
+        return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
+    if (!x || !wt || !out) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!dtype_ok(d->in_dtype) || !dtype_ok(d->out_dtype))
         return fail(OLLIE_EDTYPE, "in_dtype/out_dtype must be OLLIE_F32 or OLLIE_BF16");
-    size_t need = conv_ws(d, flags);
+    if (fused_path(d, transposed, ho, wo, flags)) {
+        if (!aligned16(x) || !aligned16(wt) || !aligned16(out))
+            return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+        hipError_t e = launch_conv_fused(conv_geom(d, ho, wo), transposed, x, wt, out,
+                                         d->out_dtype == OLLIE_BF16, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "fused GEMM+eOperator launch");
+        return OLLIE_OK;
+    }
+    if (!ws) return fail(OLLIE_EINVAL, "null workspace pointer (the two-stage path needs Y)");
+    size_t need = conv_ws(d, transposed, ho, wo, flags);
     if (ws_bytes < need)
         return fail(OLLIE_EWORKSPACE, "workspace too small: need %zu bytes, got %zu", need,
                     ws_bytes);
@@ -195,7 +213,7 @@ int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, 
 size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags) {
     int64_t ho, wo;
     if (check_conv_geom(desc, transposed ? 1 : 0, &ho, &wo)) return 0;
-    return conv_ws(desc, flags);
+    return conv_ws(desc, transposed ? 1 : 0, ho, wo, flags);
 }
 
 size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags) {

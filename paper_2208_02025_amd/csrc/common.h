@@ -62,6 +62,25 @@ template <> struct In<bf16_t> {
     }
 };
 
+// ------------------------------------------------- shared GEMM-tile building blocks
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kTileK = 64;                 // bf16 k-tile depth (128 bytes per row)
+constexpr int kTileChunks = kTileK / 8;    // 16-byte chunks per tile row
+
+// LDS slot of logical 16-byte chunk `ch` of tile row `row`: an XOR swizzle that makes
+// the 16-row ds_read_b128 fragment reads of an MFMA operand bank-conflict free.
+__device__ __forceinline__ int tile_swz(int row, int ch) {
+    return row * kTileChunks + (ch ^ (row & 7));
+}
+
+// s_waitcnt with only the vector-memory counter constrained (expcnt, lgkmcnt at max).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
 // ---------------------------------------------------------------- launchers
 // Each returns the hipError_t of the launch.
 
@@ -74,6 +93,12 @@ struct ConvGeom {
 };
 
 hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, int y_bf16,
+                             void* out, int out_bf16, hipStream_t stream);
+
+// Fused GEMM + eOperator (output-stationary), bf16 operands.  Returns
+// hipErrorInvalidValue when the shape is outside what the fused kernel supports.
+bool conv_fused_supported(const ConvGeom& g, int transposed);
+hipError_t launch_conv_fused(const ConvGeom& g, int transposed, const void* x, const void* wt,
                              void* out, int out_bf16, hipStream_t stream);
 
 struct BandGeom {

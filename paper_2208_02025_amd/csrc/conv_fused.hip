@@ -1,0 +1,300 @@
+// Fused GEMM + eOperator for the derived convolution forms (expression fusion, §4.1).
+//
+// Substituting the GEMM scope Y[m][(r,s,k)] = sum_c X[m][c] Wt[r][s][k][c] into the
+// OffsetAdd eOperator (section 2) -- or into the selective add of the strided
+// transposed convolution (section 6.3) -- gives one expression per output element:
+//   out[o][k] = sum_{taps (r,s) valid for o} sum_c X[in(o,r,s)][c] * Wt[r][s][k][c]
+// i.e. one contraction over (tap, c) whose A operand is X gathered through the
+// eOperator's index map.  This kernel evaluates that fused expression output-stationary:
+// a tile of output pixels x output channels accumulates over taps and channel blocks in
+// MFMA registers, so Y never exists, not even on chip.
+//
+// Output pixels are grouped into classes that share their tap list:
+//   forward conv:     one class; input row hi = stride*ho - pad + r*dil (per-pixel
+//                     validity against the image bounds handles the zero padding);
+//   transposed conv:  one class per output residue (ho % stride, wo % stride); a tap
+//                     belongs to the class iff (ho + pad - r*dil) is divisible by the
+//                     stride, and then hi = ho/stride + (ho%stride + pad - r*dil)/stride.
+//                     Each class contracts over its own taps only, so no partial that the
+//                     selective add would drop is ever computed.
+// Both cases are  hi = alpha*i + beta_tap,  ho = oh0 + gamma*i  over class coordinates i.
+//
+// Main loop: the bf16 DMA pipeline of the GEMM stage (global_load_lds_dwordx4 into an
+// XOR-swizzled LDS ring, v_mfma_f32_16x16x32_bf16).  A rows are gathered per tap; rows
+// whose input pixel lies in the zero padding fetch a 16-byte zero chunk instead.
+#include <stdlib.h>
+
+#include "common.h"
+
+namespace ollie {
+
+namespace {
+
+constexpr int kMaxCls = 16;
+constexpr int kMaxTaps = 64;
+
+__device__ __align__(16) uint32_t kZeroChunk[4];   // 16 zero bytes (zero-initialised)
+
+struct FusedPlan {
+    int n, c, h, w, k, ho, wo;
+    int alpha_h, alpha_w;     // input coordinate = alpha * class coordinate + beta_tap
+    int gam_h, gam_w;         // output coordinate = o0 + gamma * class coordinate
+    int tiles_n;              // output-channel tiles
+    int ncls;
+    int cls_tile0[kMaxCls + 1];   // first workgroup tile of each class
+    int cls_hc[kMaxCls], cls_wc[kMaxCls], cls_oh0[kMaxCls], cls_ow0[kMaxCls];
+    int cls_tap0[kMaxCls + 1];    // first tap of each class
+    int tap_bh[kMaxTaps], tap_bw[kMaxTaps], tap_rs[kMaxTaps];
+};
+
+template <int BM, int BN, int NSTAGE, typename OT>
+__global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void conv_fused_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt, OT* __restrict__ out,
+    FusedPlan P) {
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    constexpr int STAGE_CHUNKS = (BM + BN) * kTileChunks;
+    constexpr int LOADS = STAGE_CHUNKS / 256;
+    constexpr int A_LOADS = BM * kTileChunks / 256;
+    static_assert(STAGE_CHUNKS % 256 == 0 && (BM * kTileChunks) % 256 == 0, "whole wave loads");
+    __shared__ u32x4 lds[NSTAGE * STAGE_CHUNKS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int nblk = gridDim.x;
+    const int bid = blockIdx.x;
+    const int id = (nblk & 7) == 0 ? (bid & 7) * (nblk >> 3) + (bid >> 3) : bid;
+    int cls = 0;
+    while (cls + 1 < P.ncls && id >= P.cls_tile0[cls + 1]) ++cls;
+    const int local = id - P.cls_tile0[cls];
+    const int tm = local / P.tiles_n, tn = local % P.tiles_n;
+    const int hc = P.cls_hc[cls], wc = P.cls_wc[cls];
+    const int plane = hc * wc;
+    const int mc = P.n * plane;                 // output pixels of this class
+    const int m0 = tm * BM, k0 = tn * BN;
+    const int tap0 = P.cls_tap0[cls];
+    const int ntap = P.cls_tap0[cls + 1] - tap0;
+    const int kc_n = P.c / kTileK;
+    const int total = ntap * kc_n;
+    const int H = P.h, W = P.w, C = P.c, K = P.k;
+
+    // this lane's A rows: image base pixel and the class coordinates scaled by alpha
+    int pbase[A_LOADS], hi0[A_LOADS], wi0[A_LOADS];
+    bool rowok[A_LOADS];
+#pragma unroll
+    for (int i = 0; i < A_LOADS; ++i) {
+        const int row = (i * 4 + wave) * 8 + (lane >> 3);
+        const int m = m0 + row;
+        rowok[i] = m < mc;
+        const int mm = m < mc ? m : 0;
+        const int nn = mm / plane, rem = mm - nn * plane;
+        const int ii = rem / wc, jj = rem - ii * wc;
+        pbase[i] = nn * H * W;
+        hi0[i] = P.alpha_h * ii;
+        wi0[i] = P.alpha_w * jj;
+    }
+    const bf16_t* zero = reinterpret_cast<const bf16_t*>(kZeroChunk);
+
+    auto issue = [&](int it) {
+        const int tap = tap0 + it / kc_n;
+        const int kc = it - (it / kc_n) * kc_n;
+        const int bh = P.tap_bh[tap], bw = P.tap_bw[tap], rs = P.tap_rs[tap];
+        const int buf = it % NSTAGE;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int seg = i * 4 + wave;
+            const int row = seg * 8 + (lane >> 3);
+            const int ch = (lane & 7) ^ (row & 7);
+            const bf16_t* p;
+            if (i < A_LOADS) {
+                const int hi = hi0[i] + bh, wi = wi0[i] + bw;
+                const bool ok = rowok[i] && hi >= 0 && hi < H && wi >= 0 && wi < W;
+                p = ok ? X + (int64_t)(pbase[i] + hi * W + wi) * C + kc * kTileK + ch * 8 : zero;
+            } else {
+                int kk = k0 + (row - BM);
+                kk = kk < K ? kk : K - 1;
+                p = Wt + ((int64_t)rs * K + kk) * C + kc * kTileK + ch * 8;
+            }
+            __builtin_amdgcn_global_load_lds((const void*)p,
+                                             (lds_void*)(lds + buf * STAGE_CHUNKS + seg * 64),
+                                             16, 0, 0);
+        }
+    };
+
+    f32x4 acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int s = 0; s < NSTAGE - 1; ++s)
+        if (s < total) issue(s);
+    for (int it = 0; it < total; ++it) {
+        if (it + NSTAGE - 2 < total) wait_vmcnt<(NSTAGE - 2) * LOADS>();
+        else wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();   // tile `it` is in LDS everywhere; `it - 1` is consumed
+        if (it + NSTAGE - 1 < total) issue(it + NSTAGE - 1);
+        const u32x4* la = lds + (it % NSTAGE) * STAGE_CHUNKS;
+        const u32x4* lb = la + BM * kTileChunks;
+#pragma unroll
+        for (int kk = 0; kk < kTileK / 32; ++kk) {
+            const int ch = kk * 4 + (lane >> 4);
+            bf16x8 fa[FN], fb[FM];
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+                fa[i] = __builtin_bit_cast(bf16x8,
+                                           lb[tile_swz(wn * WN + i * 16 + (lane & 15), ch)]);
+#pragma unroll
+            for (int j = 0; j < FM; ++j)
+                fb[j] = __builtin_bit_cast(bf16x8,
+                                           la[tile_swz(wm * WM + j * 16 + (lane & 15), ch)]);
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int j = 0; j < FM; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j],
+                                                                        0, 0, 0);
+        }
+    }
+
+    // acc[i][j][v] = out[pixel of class row m][k], m = m0 + wm*WM + j*16 + lane%16,
+    //                                          k = k0 + wn*WN + i*16 + 4*(lane/16) + v
+    const bool vec_ok = (K & 3) == 0;
+    const int oh0 = P.cls_oh0[cls], ow0 = P.cls_ow0[cls];
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+        const int m = m0 + wm * WM + j * 16 + (lane & 15);
+        if (m >= mc) continue;
+        const int nn = m / plane, rem = m - nn * plane;
+        const int ii = rem / wc, jj = rem - ii * wc;
+        const int64_t opix = ((int64_t)nn * P.ho + oh0 + P.gam_h * ii) * P.wo + ow0 + P.gam_w * jj;
+        OT* orow = out + opix * K;
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+            const int k = k0 + wn * WN + i * 16 + 4 * (lane >> 4);
+            if (vec_ok && k + 3 < K) {
+                Out<OT>::put4(orow + k, acc[i][j]);
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (k + v < K) Out<OT>::put(orow + k + v, acc[i][j][v]);
+            }
+        }
+    }
+}
+
+// Host-side plan: classes, their tap lists, and the tile count for a BM x BN tiling.
+bool make_plan(const ConvGeom& g, int transposed, FusedPlan& P) {
+    P = FusedPlan{};
+    P.n = (int)g.n; P.c = (int)g.c; P.h = (int)g.h; P.w = (int)g.w; P.k = (int)g.k;
+    P.ho = (int)g.ho; P.wo = (int)g.wo;
+    int ntaps = 0, ncls = 0;
+    if (!transposed) {
+        P.alpha_h = g.sh; P.alpha_w = g.sw; P.gam_h = 1; P.gam_w = 1;
+        P.cls_hc[0] = (int)g.ho; P.cls_wc[0] = (int)g.wo; P.cls_oh0[0] = 0; P.cls_ow0[0] = 0;
+        P.cls_tap0[0] = 0;
+        for (int r = 0; r < g.r; ++r)
+            for (int s = 0; s < g.s; ++s) {
+                if (ntaps >= kMaxTaps) return false;
+                P.tap_bh[ntaps] = -g.ph + r * g.dh;
+                P.tap_bw[ntaps] = -g.pw + s * g.dw;
+                P.tap_rs[ntaps] = (int)(r * g.s + s);
+                ++ntaps;
+            }
+        ncls = 1;
+        P.cls_tap0[1] = ntaps;
+    } else {
+        P.alpha_h = 1; P.alpha_w = 1; P.gam_h = g.sh; P.gam_w = g.sw;
+        if ((int64_t)g.sh * g.sw > kMaxCls) return false;
+        for (int ah = 0; ah < g.sh; ++ah)
+            for (int aw = 0; aw < g.sw; ++aw) {
+                const int hc = ah < g.ho ? (int)((g.ho - ah + g.sh - 1) / g.sh) : 0;
+                const int wc = aw < g.wo ? (int)((g.wo - aw + g.sw - 1) / g.sw) : 0;
+                if (hc == 0 || wc == 0) continue;
+                P.cls_hc[ncls] = hc; P.cls_wc[ncls] = wc;
+                P.cls_oh0[ncls] = ah; P.cls_ow0[ncls] = aw;
+                P.cls_tap0[ncls] = ntaps;
+                for (int r = 0; r < g.r; ++r) {
+                    const int th = ah + g.ph - r * g.dh;       // divisible by sh for a class tap
+                    if (((th % g.sh) + g.sh) % g.sh != 0) continue;
+                    for (int s = 0; s < g.s; ++s) {
+                        const int tw = aw + g.pw - s * g.dw;
+                        if (((tw % g.sw) + g.sw) % g.sw != 0) continue;
+                        if (ntaps >= kMaxTaps) return false;
+                        P.tap_bh[ntaps] = th / g.sh;            // exact: th is a multiple of sh
+                        P.tap_bw[ntaps] = tw / g.sw;
+                        P.tap_rs[ntaps] = (int)(r * g.s + s);
+                        ++ntaps;
+                    }
+                }
+                ++ncls;
+            }
+        P.cls_tap0[ncls] = ntaps;
+    }
+    P.ncls = ncls;
+    return ncls > 0;
+}
+
+int64_t plan_tiles(FusedPlan& P, int bm, int bn) {
+    P.tiles_n = (P.k + bn - 1) / bn;
+    int64_t t = 0;
+    for (int c = 0; c < P.ncls; ++c) {
+        P.cls_tile0[c] = (int)t;
+        const int64_t mc = (int64_t)P.n * P.cls_hc[c] * P.cls_wc[c];
+        t += ((mc + bm - 1) / bm) * P.tiles_n;
+    }
+    P.cls_tile0[P.ncls] = (int)t;
+    return t;
+}
+
+template <int BM, int BN, int NS, typename OT>
+hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, hipStream_t st) {
+    const int64_t tiles = plan_tiles(P, BM, BN);
+    if (tiles == 0) return hipSuccess;
+    hipLaunchKernelGGL((conv_fused_kernel<BM, BN, NS, OT>), dim3((unsigned)tiles), dim3(256), 0,
+                       st, (const bf16_t*)x, (const bf16_t*)wt, (OT*)out, P);
+    return hipGetLastError();
+}
+
+// 0 = 128x128 (two workgroups per CU), 1 = 64x128, 2 = 64x64; OLLIE_FUSED_CONFIG
+// overrides the shape-based choice for tuning sweeps.
+template <typename OT>
+hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, hipStream_t st) {
+    static const int forced = [] {
+        const char* e = getenv("OLLIE_FUSED_CONFIG");
+        return e ? atoi(e) : -1;
+    }();
+    int cfg = forced;
+    if (cfg < 0 || cfg > 2) {
+        FusedPlan tmp = P;
+        if (plan_tiles(tmp, 128, 128) >= 240) cfg = 0;
+        else if (plan_tiles(tmp, 64, 128) >= 240) cfg = 1;
+        else cfg = 2;
+    }
+    switch (cfg) {
+    case 0: return go<128, 128, 2, OT>(P, x, wt, out, st);
+    case 1: return go<64, 128, 2, OT>(P, x, wt, out, st);
+    default: return go<64, 64, 2, OT>(P, x, wt, out, st);
+    }
+}
+
+}  // namespace
+
+bool conv_fused_supported(const ConvGeom& g, int transposed) {
+    if (g.c % kTileK != 0) return false;
+    FusedPlan P;
+    return make_plan(g, transposed, P);
+}
+
+hipError_t launch_conv_fused(const ConvGeom& g, int transposed, const void* x, const void* wt,
+                             void* out, int out_bf16, hipStream_t stream) {
+    FusedPlan P;
+    if (g.c % kTileK != 0 || !make_plan(g, transposed, P)) return hipErrorInvalidValue;
+    return out_bf16 ? dispatch<bf16_t>(P, x, wt, out, stream)
+                    : dispatch<float>(P, x, wt, out, stream);
+}
+
+}  // namespace ollie

@@ -28,14 +28,10 @@ namespace ollie {
 
 namespace {
 
-constexpr int kBK = 64;            // bf16 k-tile depth (128 bytes per row)
-constexpr int kChunks = kBK / 8;   // 16-byte chunks per tile row
+constexpr int kBK = kTileK;
+constexpr int kChunks = kTileChunks;
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-__device__ __forceinline__ int swz(int row, int ch) {
-    return row * kChunks + (ch ^ (row & 7));
-}
+__device__ __forceinline__ int swz(int row, int ch) { return tile_swz(row, ch); }
 
 // XCD-aware tile order: consecutive workgroup ids are dealt round-robin to the 8 XCDs.
 // Remap so that each XCD receives a contiguous range of tiles (which then share
@@ -55,13 +51,6 @@ __device__ __forceinline__ void tile_of(int bid, int nblk, int tiles_m, int tile
     int in_group = id - group * group_m * tiles_n;
     tm = first_m + in_group % gsize;
     tn = in_group / gsize;
-}
-
-// s_waitcnt with only the vector-memory counter constrained (expcnt, lgkmcnt at max).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
 }
 
 // Epilogue: acc[i][j][v] = Y[m][n], m = m0 + row0 + j*16 + lane%16,

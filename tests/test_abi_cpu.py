@@ -187,3 +187,15 @@ def test_python_binding_refuses_cpu_tensors():
     q = torch.zeros(1, 8, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         ol.banded_bmm(q, q, q, 2, 1)
+
+
+def test_fused_workspace_sizes(lib):
+    d = conv(n=16, c=256, k=256)
+    assert ol.conv_workspace_bytes(d, False, ol.FUSE_EPILOGUE) == 0
+    assert ol.conv_workspace_bytes(d, False, 0) == 16 * 14 * 14 * 9 * 256 * 4
+    d = conv(n=2, c=72, k=16)                      # c % 64 != 0: two-stage path
+    assert ol.conv_workspace_bytes(d, False, ol.FUSE_EPILOGUE) == 2 * 14 * 14 * 9 * 16 * 4
+    d = conv(n=1, c=64, k=16, in_dtype=ol.F32)     # fp32 inputs: two-stage path
+    assert ol.conv_workspace_bytes(d, False, ol.FUSE_EPILOGUE) > 0
+    d = conv(n=16, c=512, h=8, w=8, k=256, r=4, s=4, stride=2, pad=1)
+    assert ol.conv_workspace_bytes(d, True, ol.FUSE_EPILOGUE) == 0

@@ -378,3 +378,102 @@ def test_band_scale_edge_cases(scale, mask, staged):
     k = synth.random_tensor((b, l, 64), 15001, "bf16", dist="normal")
     v = synth.random_tensor((b, l, 64), 15002, "bf16", dist="normal")
     check_band(q, k, v, w, dil, scale, mask, staged)
+
+
+# ------------------------------------------------------- fused GEMM + eOperator path
+
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+@pytest.mark.parametrize("integer", [True, False])
+def test_workload_fused(cfg, integer):
+    """The fused expression (no Y) on the three convolution workloads."""
+    wl = synth.WORKLOADS[cfg]
+    say("workload", cfg, "fused integer=%s" % integer)
+    x, wt = synth.conv_inputs(wl, integer=integer, seed_offset=40)
+    xg, wg = x.to(DEV), wt.to(DEV)
+    desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), wl.stride, wl.pad, wl.dil, wl.out_pad,
+                        x.dtype, torch.float32)
+    assert ol.conv_workspace_bytes(desc, wl.transposed, ol.FUSE_EPILOGUE) == 0
+    if wl.kind == "conv2d":
+        out = ol.derived_conv2d(xg, wg, wl.stride, wl.pad, fuse=True)
+    elif wl.kind == "dilated_conv2d":
+        out = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, fuse=True)
+    else:
+        out = ol.derived_conv_transpose2d(xg, wg, wl.stride, wl.pad, wl.out_pad, wl.dil,
+                                          fuse=True)
+    torch.cuda.synchronize()
+    ref = oracle_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil, wl.out_pad)
+    if integer:
+        assert np.array_equal(to_np(out), ref)
+    else:
+        assert err(to_np(out), ref) <= TOL_BF16
+
+
+# c % 64 == 0 so the fused kernel takes them; ragged pixel counts and channel counts,
+# strides, dilations, and transposed cases whose residue classes have 0, 1 or 2 taps.
+SMALL_FUSED = [
+    ("conv2d", 3, 64, 13, 11, 20, 3, 3, (1, 1), (1, 1), (1, 1), (0, 0)),
+    ("conv2d", 1, 128, 17, 19, 36, 3, 2, (2, 1), (0, 1), (1, 1), (0, 0)),
+    ("conv2d", 2, 64, 5, 6, 7, 5, 5, (1, 1), (4, 4), (1, 1), (0, 0)),
+    ("dilated_conv2d", 1, 64, 21, 18, 12, 3, 3, (1, 1), (3, 2), (3, 2), (0, 0)),
+    ("dilated_conv2d", 2, 128, 10, 10, 130, 3, 3, (2, 2), (2, 2), (2, 2), (0, 0)),
+    ("conv_transpose2d", 3, 64, 5, 6, 12, 4, 4, (2, 2), (1, 1), (1, 1), (1, 0)),
+    ("conv_transpose2d", 1, 64, 9, 7, 8, 3, 2, (3, 2), (1, 1), (1, 2), (2, 1)),
+    ("conv_transpose2d", 2, 128, 4, 4, 5, 2, 2, (1, 1), (0, 0), (1, 1), (0, 0)),
+    ("conv_transpose2d", 1, 64, 3, 5, 16, 1, 1, (3, 3), (0, 0), (1, 1), (2, 2)),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(SMALL_FUSED)))
+@pytest.mark.parametrize("integer", [True, False])
+def test_small_shapes_fused(ci, integer):
+    kind, n, c, h, w, k, r, s, st, pd, dl, op = SMALL_FUSED[ci]
+    say("small fused", SMALL_FUSED[ci], integer)
+    x = synth.random_tensor((n, h, w, c), 16000 + ci, "bf16", integer=integer, dist="normal")
+    wt = synth.random_tensor((r, s, k, c), 17000 + ci, "bf16", integer=integer, dist="normal")
+    xg, wg = x.to(DEV), wt.to(DEV)
+    desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), st, pd, dl, op, x.dtype,
+                        torch.float32)
+    assert ol.conv_workspace_bytes(desc, kind == "conv_transpose2d", ol.FUSE_EPILOGUE) == 0
+    if kind == "conv2d":
+        out = ol.derived_conv2d(xg, wg, st, pd, fuse=True)
+    elif kind == "dilated_conv2d":
+        out = ol.derived_dilated_conv2d(xg, wg, st, pd, dl, fuse=True)
+    else:
+        out = ol.derived_conv_transpose2d(xg, wg, st, pd, op, dl, fuse=True)
+    torch.cuda.synchronize()
+    ref = oracle_conv(kind, x, wt, st, pd, dl, op)
+    if integer:
+        assert np.array_equal(to_np(out), ref)
+    else:
+        assert err(to_np(out), ref) <= TOL_BF16
+
+
+def test_fused_flag_falls_back_to_two_stages():
+    """c % 64 != 0: the fused kernel does not cover the shape, the call takes the
+    two-stage path (and needs its workspace)."""
+    kind, n, c, h, w, k, r, s, st, pd, dl, op = SMALL_BF16[0]
+    say("fused fallback", SMALL_BF16[0])
+    x = synth.random_tensor((n, h, w, c), 18000, "bf16", integer=True)
+    wt = synth.random_tensor((r, s, k, c), 18001, "bf16", integer=True)
+    desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), st, pd, dl, op, x.dtype,
+                        torch.float32)
+    assert ol.conv_workspace_bytes(desc, False, ol.FUSE_EPILOGUE) == \
+        ol.conv_workspace_bytes(desc, False, 0) > 0
+    out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), st, pd, fuse=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out), oracle_conv(kind, x, wt, st, pd, dl, op))
+
+
+def test_fused_bf16_output_and_determinism():
+    wl = synth.WORKLOADS[4]
+    say("fused bf16 out + determinism, workload 4")
+    x, wt = synth.conv_inputs(wl, seed_offset=50)
+    xg, wg = x.to(DEV), wt.to(DEV)
+    a = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, fuse=True)
+    b = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, fuse=True)
+    o16 = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, fuse=True,
+                                    out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    ref = oracle_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil)
+    assert err(to_np(o16), ref) <= TOL_BF16
