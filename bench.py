@@ -4,14 +4,17 @@ One step = one pass of the whole path over one batch of the four measured worklo
 through the public entry points, inputs already resident in HBM:
   derived_conv2d            ResNet conv3x3, N=16, C=K=256, 14x14            (GEMM + OffsetAdd)
   derived_conv_transpose2d  DCGAN convT 4x4 s2, N=16, 512->256, 8x8 -> 16x16 (GEMM + selective add)
-  derived_dilated_conv2d    CSRNet dilated conv3x3 d2, C=K=512, 96x128       (GEMM + dilated OffsetAdd)
+  derived_dilated_conv2d    CSRNet dilated conv3x3 d2, C=K=512, 96x128       (fused GEMM+OffsetAdd)
   banded_bmm                Longformer band, B=96, L=4096, d=64, w=256, dil 2 (fused G2BMM/softmax/GBMM)
+Each convolution runs the derived program variant that is faster for it (PATHS below);
+both variants are timed and reported.
 
 `value` is the step's algorithmic TFLOP/s (all GEMM-stage and band contractions over
 the step time).  Per workload it also reports the GEMM stage in TFLOP/s and % of the
-bf16 MFMA peak and the eOperator stage in GB/s and % of the HBM peak, each timed with
-HIP events around K back-to-back launches of that stage's kernel on the stream it runs
-on.  `roofline` covers the kernel that takes the largest share of a step.
+bf16 MFMA peak, the eOperator stage in GB/s and % of the HBM peak, and the fused
+kernel in TFLOP/s.  Each kernel is timed with HIP events around a HIP graph of
+back-to-back launches of that kernel (so host launch gaps do not count) on the stream
+it runs on.  `roofline` covers the kernel that takes the largest share of a step.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workloads.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
@@ -33,6 +36,32 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+# derived-program variant per convolution workload: "staged" = GEMM stage + eOperator
+# through the Y scope, "fused" = the fused expression (no Y)
+PATHS = {2: "staged", 3: "staged", 4: "fused"}
+
+
+def traffic_record(kernel_key):
+    """HBM bytes per launch of `kernel_key` ("name[workload]") from its rocprofv3 PMC
+    record in profiles/, or None when there is none or the kernel source has changed
+    since the counters were taken (the record stores the source's sha256)."""
+    import hashlib
+    kname, wl = kernel_key[:-1].split("[")
+    path = os.path.join(ROOT, "profiles", f"{kname}__{wl}__traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if ":" in line:
+            key, val = line.split(":", 1)
+            rec[key.strip()] = val.strip().split()[0] if val.strip() else ""
+    src = os.path.join(ROOT, rec.get("kernel_source", ""))
+    if not os.path.isfile(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("source_sha256"):
+        return None
+    return int(rec["traffic_bytes_per_launch"])
 
 
 def valid_taps_1d(n_in, n_out, r, stride, pad, dil, transposed):
@@ -101,13 +130,14 @@ def main():
         ws = torch.empty(ol.conv_workspace_bytes(desc, wl.transposed), dtype=torch.uint8,
                          device=dev)
         kw = dict(stride=wl.stride, padding=wl.pad, out=out, ws=ws)
+        fused = PATHS[cfg] == "fused"
         if cfg == 3:
             kw["output_padding"] = wl.out_pad
         if cfg == 4:
             kw["dilation"] = wl.dil
         flops, eop_bytes = conv_costs(wl, ho, wo)
         conv_ops.append(dict(cfg=cfg, wl=wl, entry=entry, x=x, wt=wt, kw=kw, desc=desc, ws=ws,
-                             out=out, flops=flops, eop_bytes=eop_bytes,
+                             out=out, flops=flops, eop_bytes=eop_bytes, fused=fused,
                              m=wl.n * wl.h * wl.w, nc=wl.r * wl.s * wl.k))
     bwl = synth.WORKLOADS[5]
     q, k, v = (t.to(dev) for t in synth.band_inputs(bwl))
@@ -126,7 +156,7 @@ def main():
         for i, op in enumerate(conv_ops):
             if evs is not None:
                 evs[i].record(stream)
-            op["entry"](op["x"], op["wt"], **op["kw"])
+            op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=op["fused"]))
         if evs is not None:
             evs[3].record(stream)
         band_call()
@@ -153,20 +183,27 @@ def main():
 
     # ------------------------------------------------ per-kernel timing (HIP events)
     def time_kernel(fn, reps):
+        """Average duration of one launch: `reps` launches captured in a HIP graph,
+        replayed between two events on the current stream."""
         fn()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(reps):
+                fn()
+        graph.replay()
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for _ in range(reps):
-            fn()
+        graph.replay()
         e1.record(stream)
         e1.synchronize()
         return e0.elapsed_time(e1) / reps   # ms per launch
 
     reps = max(args.steps, 10)
     per_cfg = {}
-    kernels = []   # (name, ms per launch, bound, achieved, peak, unit)
+    kernels = []   # (name, ms per launch, bound, achieved, peak, unit, algorithmic work)
     for op, ms_op in zip(conv_ops, op_ms):
         y = op["ws"][:op["m"] * op["nc"] * 4].view(torch.float32).view(op["m"], op["nc"])
         a = op["x"].view(op["m"], op["wl"].c)
@@ -174,24 +211,34 @@ def main():
         g_ms = time_kernel(lambda: ol.gemm_nt(a, b, out=y), reps)
         e_ms = time_kernel(lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y,
                                                  out=op["out"]), reps)
+        f_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
+                                               **dict(op["kw"], ws=None, fuse=True)), reps)
         g_tf = op["flops"] / (g_ms * 1e-3) / 1e12
         e_gb = op["eop_bytes"] / (e_ms * 1e-3) / 1e9
+        f_tf = op["flops"] / (f_ms * 1e-3) / 1e12
         name = op["wl"].name
         per_cfg[name] = {
+            "path": PATHS[op["cfg"]],
             "op_ms": round(ms_op, 5),
             "gemm_ms": round(g_ms, 5), "gemm_tflops": round(g_tf, 2),
             "gemm_pct_mfma_peak": round(100 * g_tf / PEAK_BF16_TFLOPS, 2),
             "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
             "eop_pct_hbm_peak": round(100 * e_gb / PEAK_HBM_GBS, 2),
+            "fused_ms": round(f_ms, 5), "fused_tflops": round(f_tf, 2),
+            "fused_pct_mfma_peak": round(100 * f_tf / PEAK_BF16_TFLOPS, 2),
             "gemm_gflop": round(op["flops"] / 1e9, 4), "eop_mbytes": round(op["eop_bytes"] / 1e6, 3),
         }
-        kernels.append((f"gemm_nt[{name}]", g_ms, "mfma", g_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
-                        op["flops"]))
-        kernels.append((f"eop_gather[{name}]", e_ms, "hbm", e_gb, PEAK_HBM_GBS, "GB/s",
-                        op["eop_bytes"]))
+        if op["fused"]:
+            kernels.append((f"conv_fused[{name}]", f_ms, "mfma", f_tf, PEAK_BF16_TFLOPS,
+                            "TFLOP/s", op["flops"]))
+        else:
+            kernels.append((f"gemm_nt[{name}]", g_ms, "mfma", g_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
+                            op["flops"]))
+            kernels.append((f"eop_gather[{name}]", e_ms, "hbm", e_gb, PEAK_HBM_GBS, "GB/s",
+                            op["eop_bytes"]))
     b_ms = time_kernel(band_call, reps)
     b_tf = bflops / (b_ms * 1e-3) / 1e12
-    per_cfg[bwl.name] = {"op_ms": round(op_ms[3], 5), "fused_ms": round(b_ms, 5),
+    per_cfg[bwl.name] = {"path": "fused", "op_ms": round(op_ms[3], 5), "fused_ms": round(b_ms, 5),
                          "band_tflops": round(b_tf, 2),
                          "band_pct_mfma_peak": round(100 * b_tf / PEAK_BF16_TFLOPS, 2),
                          "band_gflop": round(bflops / 1e9, 3)}
@@ -200,7 +247,7 @@ def main():
     dom = max(kernels, key=lambda t: t[1])
     roofline = {"kernel": dom[0], "bound": dom[2], "achieved": round(dom[3], 3),
                 "peak": dom[4], "unit": dom[5], "frac": round(dom[3] / dom[4], 4),
-                "traffic": None, "avg_launch_ms": round(dom[1], 5),
+                "traffic": traffic_record(dom[0]), "avg_launch_ms": round(dom[1], 5),
                 "algorithmic_per_launch": dom[6]}
 
     # ---------------------------------------------------------------- CPU baseline

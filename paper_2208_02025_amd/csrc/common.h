@@ -74,6 +74,16 @@ __device__ __forceinline__ int tile_swz(int row, int ch) {
     return row * kTileChunks + (ch ^ (row & 7));
 }
 
+// The same for a k-tile of BK bf16 (BK/8 chunks per row): 128-byte rows use the chunk
+// XOR (row & 7); 64-byte rows pair up rows and XOR (row/2 & 3), so the eight rows that
+// one ds_read_b128 phase touches still land on disjoint banks.
+template <int BK>
+__device__ __forceinline__ int tile_swz_k(int row, int ch) {
+    static_assert(BK == 32 || BK == 64, "k-tile depth");
+    if constexpr (BK == 64) return row * 8 + (ch ^ (row & 7));
+    else return row * 4 + (ch ^ ((row >> 1) & 3));
+}
+
 // s_waitcnt with only the vector-memory counter constrained (expcnt, lgkmcnt at max).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {

@@ -80,14 +80,17 @@ __device__ __forceinline__ void store_tile(YT* __restrict__ Y, const f32x4 (&acc
 }
 
 // ------------------------------------------------------------------ main bf16 path
-template <int BM, int BN, int NSTAGE, typename YT>
-__global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void gemm_nt_bf16_dma_kernel(
-    const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, YT* __restrict__ Y,
-    int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n) {
+template <int BM, int BN, int BK, int NSTAGE, typename YT>
+__global__ __launch_bounds__(256, (NSTAGE * (BM + BN) * BK * 2 <= 80 * 1024) ? 2 : 1)
+void gemm_nt_bf16_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
+                             YT* __restrict__ Y, int64_t M, int64_t N, int64_t K, int tiles_m,
+                             int tiles_n) {
     constexpr int WM = BM / 2, WN = BN / 2;        // wave sub-tile (2 x 2 waves)
     constexpr int FM = WM / 16, FN = WN / 16;      // 16x16 MFMA blocks per wave
+    constexpr int CPR = BK / 8;                    // 16-byte chunks per tile row
+    constexpr int RPI = 64 / CPR;                  // tile rows per wave-wide DMA instruction
     constexpr int ROWS = BM + BN;                  // tile rows per stage (A rows, then B rows)
-    constexpr int STAGE_CHUNKS = ROWS * kChunks;
+    constexpr int STAGE_CHUNKS = ROWS * CPR;
     constexpr int LOADS = STAGE_CHUNKS / 256;      // DMA instructions per wave per stage
     static_assert(STAGE_CHUNKS % 256 == 0, "stage must be a whole number of wave loads");
     __shared__ u32x4 lds[NSTAGE * STAGE_CHUNKS];
@@ -101,12 +104,17 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void gemm_nt_bf16_dma_ker
     const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
 
     // Per-lane source rows for this wave's DMA instructions.  Instruction i of wave w
-    // fills LDS chunk slots [(i*4 + w)*64, +64): rows (i*4+w)*8 + lane/8, slot lane%8.
+    // fills LDS chunk slots [(i*4 + w)*64, +64): rows (i*4+w)*RPI + lane/CPR, slot lane%CPR.
     const bf16_t* src[LOADS];
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
-        const int row = (i * 4 + wave) * 8 + (lane >> 3);
-        const int ch = (lane & 7) ^ (row & 7);
+        const int row = (i * 4 + wave) * RPI + lane / CPR;
+        const int slot = lane % CPR;
+        // the lane filling slot `slot` of `row` fetches the chunk the swizzle puts there
+        int ch = 0;
+#pragma unroll
+        for (int c = 0; c < CPR; ++c)
+            if (tile_swz_k<BK>(row, c) - row * CPR == slot) ch = c;
         const bf16_t* p;
         if (row < BM) {
             int64_t gm = m0 + row;
@@ -120,7 +128,7 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void gemm_nt_bf16_dma_ker
         src[i] = p;
     }
     auto issue = [&](int kt, int buf) {
-        const int64_t koff = (int64_t)kt * kBK;
+        const int64_t koff = (int64_t)kt * BK;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i)
             __builtin_amdgcn_global_load_lds(
@@ -134,7 +142,7 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void gemm_nt_bf16_dma_ker
 #pragma unroll
         for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-    const int ktiles = (int)(K / kBK);
+    const int ktiles = (int)(K / BK);
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s)
         if (s < ktiles) issue(s, s);
@@ -146,17 +154,19 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void gemm_nt_bf16_dma_ker
         __builtin_amdgcn_s_barrier();   // every wave's part of tile kt is in LDS; tile kt-1 is consumed
         if (kt + NSTAGE - 1 < ktiles) issue(kt + NSTAGE - 1, (kt + NSTAGE - 1) % NSTAGE);
         const u32x4* la = lds + (kt % NSTAGE) * STAGE_CHUNKS;
-        const u32x4* lb = la + BM * kChunks;
+        const u32x4* lb = la + BM * CPR;
 #pragma unroll
-        for (int kk = 0; kk < kBK / 32; ++kk) {
+        for (int kk = 0; kk < BK / 32; ++kk) {
             const int ch = kk * 4 + (lane >> 4);
             bf16x8 fa[FN], fb[FM];
 #pragma unroll
             for (int i = 0; i < FN; ++i)
-                fa[i] = __builtin_bit_cast(bf16x8, lb[swz(wn * WN + i * 16 + (lane & 15), ch)]);
+                fa[i] = __builtin_bit_cast(
+                    bf16x8, lb[tile_swz_k<BK>(wn * WN + i * 16 + (lane & 15), ch)]);
 #pragma unroll
             for (int j = 0; j < FM; ++j)
-                fb[j] = __builtin_bit_cast(bf16x8, la[swz(wm * WM + j * 16 + (lane & 15), ch)]);
+                fb[j] = __builtin_bit_cast(
+                    bf16x8, la[tile_swz_k<BK>(wm * WM + j * 16 + (lane & 15), ch)]);
 #pragma unroll
             for (int i = 0; i < FN; ++i)
 #pragma unroll
@@ -472,11 +482,11 @@ __global__ __launch_bounds__(256) void gemm_nt_f32_kernel(
     store_tile<2, 2, YT>(Y, acc, M, N, m0 + wm * 32, n0 + wn * 32);
 }
 
-template <int BM, int BN, int NSTAGE, typename YT>
+template <int BM, int BN, int BK, int NSTAGE, typename YT>
 hipError_t go_dma(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
                   hipStream_t stream) {
     int tiles_m = (int)((m + BM - 1) / BM), tiles_n = (int)((n + BN - 1) / BN);
-    hipLaunchKernelGGL((gemm_nt_bf16_dma_kernel<BM, BN, NSTAGE, YT>), dim3(tiles_m * tiles_n),
+    hipLaunchKernelGGL((gemm_nt_bf16_dma_kernel<BM, BN, BK, NSTAGE, YT>), dim3(tiles_m * tiles_n),
                        dim3(256), 0, stream, (const bf16_t*)a, (const bf16_t*)b, (YT*)y, m, n, k,
                        tiles_m, tiles_n);
     return hipGetLastError();
@@ -510,14 +520,16 @@ hipError_t go_persistent(int64_t m, int64_t n, int64_t k, const void* a, const v
 
 // Tile configuration of the DMA kernels: 0 = 256x128, 3 stages (one workgroup per CU);
 // 1 = 128x128, 3 stages (one per CU); 2 = 128x128, 2 stages (two per CU);
-// 3 = persistent 256x256, 2 stages, 8 waves; 4 = persistent 256x128, 3 stages, 4 waves.
-// OLLIE_GEMM_CONFIG (0..4) overrides the shape-based choice, for tuning sweeps.
+// 3 = persistent 256x256, 2 stages, 8 waves; 4 = persistent 256x128, 3 stages, 4 waves;
+// 5 = 128x256 and 6 = 256x128 with 32-deep k-tiles, 3 stages (two workgroups per CU);
+// 7 = 128x128, 32-deep k-tiles, 4 stages.
+// OLLIE_GEMM_CONFIG (0..7) overrides the shape-based choice, for tuning sweeps.
 int pick_config(int64_t m, int64_t n) {
     static const int forced = [] {
         const char* e = getenv("OLLIE_GEMM_CONFIG");
         return e ? atoi(e) : -1;
     }();
-    if (forced >= 0 && forced <= 4) return forced;
+    if (forced >= 0 && forced <= 7) return forced;
     const int64_t t128 = ((m + 127) / 128) * ((n + 127) / 128);
     if (t128 > 256) return 2;           // two workgroups per CU hide each other's latency
     return 1;
@@ -532,9 +544,12 @@ hipError_t go_bf16(int64_t m, int64_t n, int64_t k, const void* a, const void* b
         switch (cfg) {
         case 3: return go_persistent<256, 256, 2, 2, 4, YT>(m, n, k, a, b, y, stream);
         case 4: return go_persistent<256, 128, 3, 2, 2, YT>(m, n, k, a, b, y, stream);
-        case 0: return go_dma<256, 128, 3, YT>(m, n, k, a, b, y, stream);
-        case 1: return go_dma<128, 128, 3, YT>(m, n, k, a, b, y, stream);
-        default: return go_dma<128, 128, 2, YT>(m, n, k, a, b, y, stream);
+        case 0: return go_dma<256, 128, 64, 3, YT>(m, n, k, a, b, y, stream);
+        case 1: return go_dma<128, 128, 64, 3, YT>(m, n, k, a, b, y, stream);
+        case 5: return go_dma<128, 256, 32, 3, YT>(m, n, k, a, b, y, stream);
+        case 6: return go_dma<256, 128, 32, 3, YT>(m, n, k, a, b, y, stream);
+        case 7: return go_dma<128, 128, 32, 4, YT>(m, n, k, a, b, y, stream);
+        default: return go_dma<128, 128, 64, 2, YT>(m, n, k, a, b, y, stream);
         }
     }
     int tiles_m = (int)((m + 127) / 128), tiles_n = (int)((n + 127) / 128);
