@@ -314,11 +314,18 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
     for _ in range(args.warmup):
         fn()
     torch.cuda.synchronize()
+    # a HIP graph of `steps` launches, replayed between two events: kernel time only,
+    # no host launch gaps (the same method as the main benchmark's per-kernel figures)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(args.steps):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record(stream)
-    for _ in range(args.steps):
-        fn()
+    graph.replay()
     e1.record(stream)
     e1.synchronize()
     print(json.dumps({"stage": name, "launches": args.steps,

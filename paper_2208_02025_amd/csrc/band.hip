@@ -24,6 +24,8 @@
 // returns one column (value dimension) across four keys.
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace ollie {
@@ -336,9 +338,14 @@ __global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGe
         t.lr = ((int)g.l - t.rho + g.dil - 1) / g.dil;
         if (t.q0 >= t.lr) return;
     }
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
+    // the wave index through readfirstlane: every per-wave block test below is then a
+    // scalar branch rather than an exec-masked one
+    const int lane = threadIdx.x & 63, grp = lane >> 4;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int w = (int)g.w;
     const int qa = t.q0 + wv * kQPW;      // the wave's first query
+    // byte addresses of the lanes 16 and 32 apart, for the 4-lane row reductions
+    const int xor16 = (lane ^ 16) << 2, xor32 = (lane ^ 32) << 2;
     const float sl2 = fabsf(g.scale) * 1.4426950408889634f;
     const uint32_t qflip = g.scale < 0.f ? 0x80008000u : 0u;
 
@@ -378,20 +385,30 @@ __global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGe
     int tt0 = t.q0 - w + r0;                                     // subsequence row of chunk 0
     int64_t off0 = ((int64_t)t.b * g.l + t.rho) * kD + (int64_t)tt0 * g.dil * kD + ch * 8;
     KVRegs r;
+    int blk0 = t.q0 - w;                                         // first key of the next block
     auto gload = [&]() {
+        if (blk0 >= 0 && blk0 + kT <= t.lr) {                    // whole block in range
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const int tt = tt0 + 32 * e;
-            u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-            if (tt >= 0 && tt < t.lr) {
-                kv = *reinterpret_cast<const u32x4*>(K + off0 + e * half_step);
-                vv = *reinterpret_cast<const u32x4*>(V + off0 + e * half_step);
+            for (int e = 0; e < 2; ++e) {
+                r.k[e] = *reinterpret_cast<const u32x4*>(K + off0 + e * half_step);
+                r.v[e] = *reinterpret_cast<const u32x4*>(V + off0 + e * half_step);
             }
-            r.k[e] = kv;
-            r.v[e] = vv;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const int tt = tt0 + 32 * e;
+                u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+                if (tt >= 0 && tt < t.lr) {
+                    kv = *reinterpret_cast<const u32x4*>(K + off0 + e * half_step);
+                    vv = *reinterpret_cast<const u32x4*>(V + off0 + e * half_step);
+                }
+                r.k[e] = kv;
+                r.v[e] = vv;
+            }
         }
         tt0 += kT;
         off0 += row_step;
+        blk0 += kT;
     };
     gload();
     lstore_block<true, true>(r, lk[0], lv[0]);
@@ -406,50 +423,45 @@ __global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGe
             // per query half: does the block meet its band, and is it entirely inside?
             f32x4 s[QH][4];
             const u32x4* lkc = lk[cur];
+            bf16x8 kf[4][2];          // all key fragments first, then the MFMAs
 #pragma unroll
             for (int ft = 0; ft < 4; ++ft) {
                 const int row = ft * 16 + (lane & 15);
-                const bf16x8 k0 = __builtin_bit_cast(bf16x8, lkc[kswz(row, grp)]);
-                const bf16x8 k1 = __builtin_bit_cast(bf16x8, lkc[kswz(row, 4 + grp)]);
+                kf[ft][0] = __builtin_bit_cast(bf16x8, lkc[kswz(row, grp)]);
+                kf[ft][1] = __builtin_bit_cast(bf16x8, lkc[kswz(row, 4 + grp)]);
+            }
+#pragma unroll
+            for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
                 for (int hq = 0; hq < QH; ++hq) {
                     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[hq][0], acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[hq][1], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][0], qf[hq][0], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][1], qf[hq][1], acc, 0, 0, 0);
                     s[hq][ft] = acc;
                 }
-            }
             bf16x8 pf[QH][2];
-#pragma unroll
-            for (int hq = 0; hq < QH; ++hq) {
-                const int qh = qa + hq * 16;              // first query of this half
-                const int q = qh + (lane & 15);
-                bool full = t0 - (qh + 15) >= -w && t0 + kT - 1 - qh <= w;
-                if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
-                // live(ft, v): key t0+16ft+4grp+v is inside the query's band (and, in mask
-                // mode, inside the sequence)
-                auto live = [&](int ft, int v) {
-                    const int tt = t0 + ft * 16 + 4 * grp + v;
-                    const int dj = tt - q;
-                    bool l = dj >= -w && dj <= w;
-                    if (MASK) l = l && tt >= 0 && tt < t.lr;
-                    return l;
-                };
+            // Softmax of one 16-query half: block max (4-lane reduction), lazy rescale,
+            // then p = exp2(score * scale * log2(e) - m) packed to bf16.  Full blocks and
+            // masked blocks run separate copies, so no mask arithmetic reaches full blocks.
+            auto soft = [&](int hq, auto masked) {
+                constexpr bool M = decltype(masked)::value;
+                const int q = qa + hq * 16 + (lane & 15);
                 float mb = -INFINITY;
-                if (full) {
 #pragma unroll
-                    for (int ft = 0; ft < 4; ++ft)
+                for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) mb = fmaxf(mb, s[hq][ft][v]);
-                } else {
-#pragma unroll
-                    for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            if (live(ft, v)) mb = fmaxf(mb, s[hq][ft][v]);
-                }
-                mb = fmaxf(mb, __shfl_xor(mb, 16));
-                mb = fmaxf(mb, __shfl_xor(mb, 32));
+                    for (int v = 0; v < 4; ++v) {
+                        if constexpr (M) {
+                            const int tt = t0 + ft * 16 + 4 * grp + v;
+                            const int dj = tt - q;
+                            bool l = dj >= -w && dj <= w;
+                            if (MASK) l = l && tt >= 0 && tt < t.lr;
+                            if (!l) s[hq][ft][v] = -INFINITY;
+                        }
+                        mb = fmaxf(mb, s[hq][ft][v]);
+                    }
+                mb = fmaxf(mb, __int_as_float(__builtin_amdgcn_ds_bpermute(xor16, __float_as_int(mb))));
+                mb = fmaxf(mb, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32, __float_as_int(mb))));
                 const float mbx = mb * sl2;               // block max in log2 units
                 const bool need = mbx > m_run[hq] + kLazy;
                 if (__any(need)) {
@@ -469,20 +481,27 @@ __global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGe
                         float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h][v], sl2, nm));
                         float p1 =
                             __builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h + 1][v], sl2, nm));
-                        if (!full) {
-                            p0 = live(2 * h, v) ? p0 : 0.f;
-                            p1 = live(2 * h + 1, v) ? p1 : 0.f;
+                        if constexpr (M) {   // -inf * 0 (scale 0) must still give p = 0
+                            p0 = s[hq][2 * h][v] == -INFINITY ? 0.f : p0;
+                            p1 = s[hq][2 * h + 1][v] == -INFINITY ? 0.f : p1;
                         }
                         pv[v] = (__bf16)p0;
                         pv[4 + v] = (__bf16)p1;
                     }
                     pf[hq][h] = pv;
                 }
+            };
+#pragma unroll
+            for (int hq = 0; hq < QH; ++hq) {
+                const int qh = qa + hq * 16;              // first query of this half
+                bool full = t0 - (qh + 15) >= -w && t0 + kT - 1 - qh <= w;
+                if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
+                if (full) soft(hq, std::false_type{});
+                else soft(hq, std::true_type{});
             }
             // O^T += V^T P^T and the denominator += 1^T P^T, over the block's keys
-            const bf16_t* lvc = lv[cur];
             const int li = lane & 15;
-            const bf16_t* base = lvc + (4 * grp + (li >> 2)) * kVLd + 4 * (li & 3);
+            const bf16_t* base = lv[cur] + (4 * grp + (li >> 2)) * kVLd + 4 * (li & 3);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
 #pragma unroll

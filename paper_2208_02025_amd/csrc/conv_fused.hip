@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void conv_fused_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int nblk = gridDim.x;
     const int bid = blockIdx.x;

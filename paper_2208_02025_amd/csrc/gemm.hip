@@ -97,7 +97,7 @@ void gemm_nt_bf16_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restr
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
     tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_nt_bf16_persis
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int ntiles = tiles_m * tiles_n;
     const int G = gridDim.x;
@@ -350,7 +350,7 @@ __global__ __launch_bounds__(256) void gemm_nt_bf16_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
     tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
@@ -440,7 +440,7 @@ __global__ __launch_bounds__(256) void gemm_nt_f32_kernel(
     __shared__ float lb[BN * LD];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
     const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
