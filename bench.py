@@ -152,32 +152,36 @@ def main():
         run_stage(args, conv_ops, bwl, q, k, v, o, stream)
         return
 
-    def step(evs=None):
-        for i, op in enumerate(conv_ops):
-            if evs is not None:
-                evs[i].record(stream)
+    def step():
+        for op in conv_ops:
             op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=op["fused"]))
-        if evs is not None:
-            evs[3].record(stream)
         band_call()
-        if evs is not None:
-            evs[4].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     # ----------------------------------------------------------------- timed steps
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # K steps launched back to back on one stream: the host stays ahead of the GPU, so
+    # the kernels of consecutive steps run without gaps.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
+    for _ in range(args.steps):
+        step()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-    op_ms = [sum(evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)) / args.steps
-             for j in range(4)]
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    # The same step captured once into a HIP graph and replayed K times (for callers that
+    # replay a graph per batch); each replay adds the graph launch latency between steps.
+    step_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(step_graph):
+        step()
+    step_graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step_graph.replay()
+    torch.cuda.synchronize()
+    graph_ms = (time.perf_counter() - t0) * 1e3 / args.steps
     total_flops = sum(op["flops"] for op in conv_ops) + bflops
     value = total_flops / (ms_per_step * 1e-3) / 1e12
 
@@ -204,7 +208,7 @@ def main():
     reps = max(args.steps, 10)
     per_cfg = {}
     kernels = []   # (name, ms per launch, bound, achieved, peak, unit, algorithmic work)
-    for op, ms_op in zip(conv_ops, op_ms):
+    for op in conv_ops:
         y = op["ws"][:op["m"] * op["nc"] * 4].view(torch.float32).view(op["m"], op["nc"])
         a = op["x"].view(op["m"], op["wl"].c)
         b = op["wt"].view(op["nc"], op["wl"].c)
@@ -219,7 +223,7 @@ def main():
         name = op["wl"].name
         per_cfg[name] = {
             "path": PATHS[op["cfg"]],
-            "op_ms": round(ms_op, 5),
+            "op_ms": round(f_ms if op["fused"] else g_ms + e_ms, 5),
             "gemm_ms": round(g_ms, 5), "gemm_tflops": round(g_tf, 2),
             "gemm_pct_mfma_peak": round(100 * g_tf / PEAK_BF16_TFLOPS, 2),
             "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
@@ -238,7 +242,7 @@ def main():
                             op["eop_bytes"]))
     b_ms = time_kernel(band_call, reps)
     b_tf = bflops / (b_ms * 1e-3) / 1e12
-    per_cfg[bwl.name] = {"path": "fused", "op_ms": round(op_ms[3], 5), "fused_ms": round(b_ms, 5),
+    per_cfg[bwl.name] = {"path": "fused", "op_ms": round(b_ms, 5), "fused_ms": round(b_ms, 5),
                          "band_tflops": round(b_tf, 2),
                          "band_pct_mfma_peak": round(100 * b_tf / PEAK_BF16_TFLOPS, 2),
                          "band_gflop": round(bflops / 1e9, 3)}
@@ -258,12 +262,14 @@ def main():
     line = {
         "metric": "GEMM TFLOP/s (% MFMA peak) + eOperator GB/s (% HBM peak), per config, 1 GPU",
         "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "graph_replay_ms_per_step": round(graph_ms, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "derived conv3x3 (N16 C256 14x14) + convT4x4s2 (N16 512->256 "
                                "8x8) + dilated conv3x3 d2 (C512 96x128) + band (B96 L4096 d64 "
                                "w256 dil2), bf16 in, fp32 accumulate/out",
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU", "launch": "stream",
+                   "paths": {synth.WORKLOADS[c].name: p for c, p in PATHS.items()}},
         "per_config": per_cfg,
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -333,34 +339,38 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
 
 
 def cpu_baseline(conv_ops, bwl):
-    """The oracle (as it stands) on one whole step of the same workloads: every output
-    of the three convolutions and every row of the band (about 10-20 s on a 16-core
-    host); value = the step's algorithmic flops / CPU time."""
+    """The oracle (as it stands) on whole steps of the same workloads: every output of
+    the three convolutions and every row of the band, repeated until about 10 s of CPU
+    time (at most 8 steps); value = the steps' algorithmic flops / CPU time."""
     import oracle
     import synth
 
+    inputs = [(op, synth.conv_inputs(op["wl"])) for op in conv_ops]
+    qkv = synth.band_inputs(bwl)
     flops = 0.0
     secs = 0.0
-    for op in conv_ops:
-        wl = op["wl"]
-        x, wt = synth.conv_inputs(wl)
+    steps = 0
+    while steps == 0 or (secs < 10.0 and steps < 8):
+        for op, (x, wt) in inputs:
+            wl = op["wl"]
+            t0 = time.perf_counter()
+            if wl.transposed:
+                oracle.conv_transpose2d(x, wt, wl.stride, wl.pad, wl.dil, wl.out_pad)
+            else:
+                oracle.conv2d(x, wt, wl.stride, wl.pad, wl.dil)
+            secs += time.perf_counter() - t0
+            flops += op["flops"]
         t0 = time.perf_counter()
-        if wl.transposed:
-            oracle.conv_transpose2d(x, wt, wl.stride, wl.pad, wl.dil, wl.out_pad)
-        else:
-            oracle.conv2d(x, wt, wl.stride, wl.pad, wl.dil)
+        oracle.band(*qkv, bwl.w, bwl.dilation, bwl.scale, bwl.mask_invalid, want_s=False,
+                    want_p=False)
         secs += time.perf_counter() - t0
-        flops += op["flops"]
-    q, k, v = synth.band_inputs(bwl)
-    t0 = time.perf_counter()
-    oracle.band(q, k, v, bwl.w, bwl.dilation, bwl.scale, bwl.mask_invalid, want_s=False,
-                want_p=False)
-    secs += time.perf_counter() - t0
-    flops += band_flops(bwl)
+        flops += band_flops(bwl)
+        steps += 1
     return {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle", "seconds": round(secs, 2),
-            "sample": "one whole step: all outputs of the conv3x3, convT and dilated conv "
-                      "workloads and all 393216 band rows"}
+            "sample": f"{steps} whole step(s), repeated until at least 10 s of CPU time: all "
+                      "outputs of the conv3x3, convT and dilated conv workloads and all "
+                      "393216 band rows"}
 
 
 if __name__ == "__main__":

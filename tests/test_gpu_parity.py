@@ -477,3 +477,41 @@ def test_fused_bf16_output_and_determinism():
     assert torch.equal(a, b)
     ref = oracle_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil)
     assert err(to_np(o16), ref) <= TOL_BF16
+
+
+def test_hip_graph_replays_match_eager():
+    """The library's calls captured in a HIP graph (as the benchmark does) give the
+    eager results on every replay, with eager work and synchronisations in between."""
+    say("hip graph replay vs eager")
+    wl2, wl4 = synth.WORKLOADS[2], synth.WORKLOADS[4]
+    x2, w2 = (t.to(DEV) for t in synth.conv_inputs(wl2, seed_offset=60))
+    x4, w4 = (t.to(DEV) for t in synth.conv_inputs(wl4, seed_offset=60))
+    q, k, v = (synth.random_tensor((4, 777, 64), 19000 + i, "bf16", dist="normal").to(DEV)
+               for i in range(3))
+    desc2 = ol.conv_desc(tuple(x2.shape), tuple(w2.shape), 1, 1, 1, 0, x2.dtype, torch.float32)
+    ws2 = torch.empty(ol.conv_workspace_bytes(desc2, False), dtype=torch.uint8, device=DEV)
+    o2 = torch.empty((16, 14, 14, 256), device=DEV)
+    o4 = torch.empty((1, 96, 128, 512), device=DEV)
+    ob = torch.empty((4, 777, 64), device=DEV)
+
+    def calls():
+        ol.derived_conv2d(x2, w2, 1, 1, out=o2, ws=ws2)
+        ol.derived_dilated_conv2d(x4, w4, 1, 2, 2, out=o4, fuse=True)
+        ol.banded_bmm(q, k, v, 40, 3, 0.125, out=ob)
+
+    calls()
+    torch.cuda.synchronize()
+    ref = [o2.clone(), o4.clone(), ob.clone()]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    for i in range(4):
+        for t in (o2, o4, ob):
+            t.fill_(float("nan"))
+        junk = torch.randn(1 << 20, device=DEV) * i      # unrelated eager work
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert float(junk.abs().sum()) >= 0
+        for got, exp in zip((o2, o4, ob), ref):
+            assert torch.equal(got, exp), f"replay {i} differs from the eager result"
