@@ -302,30 +302,70 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
 
 // --------------------------------------------------------------------- fused
 // G2BMM -> online softmax -> GBMM in one pass over the key blocks of the band; scores
-// and probabilities stay in registers, K/V blocks are double-buffered in LDS (the next
-// block's global loads are in flight while the current one is computed).
+// and probabilities stay in registers.  A wave owns 32 queries (two 16-query halves hq),
+// a workgroup 128.  Key/value blocks of 64 rows reach LDS by direct global->LDS copies
+// (global_load_lds_dwordx4) into a ring of kSlots blocks, issued kSlots - 1 blocks
+// ahead.  Each block iteration computes the softmax and P*V of block kb while the
+// scores of block kb + 1 are computed by MFMA between its exp2 instructions, so the
+// matrix unit and the vector ALU work side by side; the loop is unrolled by two so the
+// two score buffers alternate without register copies.
 //
-// Each wave owns QH 16-query groups; with QH = 2 every K and V fragment read from LDS
-// feeds two MFMAs (at the cost of occupancy).  Softmax bookkeeping per query, in log2 units
-// (x = scale*log2(e)*score): a running reference m, and the denominator and O both
-// accumulated unnormalised by MFMA -- the denominator as the product of an all-ones
-// operand with the same bf16 probabilities that multiply V, so O and its normaliser
-// see identical rounding.  m is raised only when a block's maximum exceeds it by more
-// than kLazy, so most blocks need no rescaling and every exp2 argument stays <= kLazy.
-// The scale enters as one FMA per score; a negative scale is handled by negating the
-// query fragments (an exact sign flip of bf16) and using |scale|.
-template <typename OT, bool MASK, int QH>
-__global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGeom g, int ntx,
-                                                        const bf16_t* __restrict__ Q,
-                                                        const bf16_t* __restrict__ K,
-                                                        const bf16_t* __restrict__ V,
-                                                        OT* __restrict__ O) {
-    constexpr float kLazy = 8.f;
-    constexpr int kQPW = 16 * QH;        // queries per wave
-    constexpr int kFT = kQPW * 4;        // queries per tile (4 waves)
-    __shared__ u32x4 lk[2][kT * 8];
-    __shared__ __attribute__((aligned(16))) bf16_t lv[2][kT * kVLd];
-    // tile geometry (kFT queries per tile)
+// Softmax bookkeeping per query, in log2 units (x = scale*log2(e)*score): a running
+// reference m, and the denominator and O both accumulated unnormalised by MFMA -- the
+// denominator as the product of an all-ones operand with the same bf16 probabilities
+// that multiply V, so O and its normaliser see identical rounding.  m is raised only
+// when a score exceeds it by more than kLazy; the test uses each lane's own maximum,
+// and only when it fires is the row maximum formed across the row's 4 lanes.  The
+// scale enters as one FMA per score; a negative scale is handled by negating the query
+// fragments (an exact sign flip of bf16) and using |scale|.  Band and range masks are
+// applied in place, only on blocks that cross an edge.
+//
+// LDS slot layout: 512 16-byte chunks of K, then 512 of V; chunk c of key row r sits
+// at r*8 + (c ^ (r & 7)) (an XOR swizzle: the 16-lane fragment reads of K and the
+// transposing reads of V then spread over all bank groups).  A DMA instruction writes
+// 64 consecutive chunks in lane order, so the swizzle is applied to the source
+// address.  Keys outside the subsequence read a 16-byte zero chunk.
+constexpr int kSlotChunks = 2 * kT * 8;
+__device__ __align__(16) uint32_t kBandZero[4];
+
+// ds_read_b64_tr_b16 as inline assembly, at LDS byte address addr + OFF.  The
+// compiler's own form of this load is treated as possibly reading the destination of
+// any global->LDS copy still in flight and waits for all of them (vmcnt(0)), which
+// would drain the prefetch ring every block; the ring schedule (vmcnt + barrier before
+// a slot is read) already guarantees the block is resident.  The compiler does not
+// track this load: its results pass through lds_wait() before any use.
+template <int OFF>
+__device__ __forceinline__ s16x4 tr_read_raw(uint32_t addr) {
+    s16x4 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+// Waits for every outstanding LDS read; the listed registers are tied to the wait, so
+// no use of them can be scheduled before it.
+__device__ __forceinline__ void lds_wait(bf16x8 (&a)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]));
+}
+
+__device__ __forceinline__ void block_sync() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <typename OT, bool MASK, int kSlots>
+__global__ __launch_bounds__(256, 2) void band_fused_kernel(BandGeom g, int ntx,
+                                                           const bf16_t* __restrict__ Q,
+                                                           const bf16_t* __restrict__ K,
+                                                           const bf16_t* __restrict__ V,
+                                                           OT* __restrict__ O) {
+    // The reference moves only when a score exceeds it by more than kLazy (log2 units), so
+    // p <= 2^kLazy: with at most 2w+1 terms per row, O and its normaliser stay far inside
+    // the fp32 range, and bf16 p keeps its relative precision at any magnitude.  A wide
+    // margin means the reference settles after the first block and rescaling is rare.
+    constexpr float kLazy = 64.f;
+    constexpr int kQW = 32;               // queries per wave
+    constexpr int kFT = 4 * kQW;          // queries per tile
+    __shared__ u32x4 lds[kSlots * kSlotChunks];
     Tile t;
     {
         const int nblk_all = gridDim.x;
@@ -338,21 +378,20 @@ __global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGe
         t.lr = ((int)g.l - t.rho + g.dil - 1) / g.dil;
         if (t.q0 >= t.lr) return;
     }
-    // the wave index through readfirstlane: every per-wave block test below is then a
-    // scalar branch rather than an exec-masked one
-    const int lane = threadIdx.x & 63, grp = lane >> 4;
+    const int lane = threadIdx.x & 63, grp = lane >> 4, li = lane & 15;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int w = (int)g.w;
-    const int qa = t.q0 + wv * kQPW;      // the wave's first query
-    // byte addresses of the lanes 16 and 32 apart, for the 4-lane row reductions
+    const int qa = t.q0 + wv * kQW;
     const int xor16 = (lane ^ 16) << 2, xor32 = (lane ^ 32) << 2;
-    const float sl2 = fabsf(g.scale) * 1.4426950408889634f;
+    // scale * log2(e), kept >= the smallest normal float: with scale 0 every score then
+    // maps to exp2(~0) = 1 exactly, and a masked score (-inf) still maps to 0
+    const float sl2 = fmaxf(fabsf(g.scale) * 1.4426950408889634f, 1.17549435e-38f);
     const uint32_t qflip = g.scale < 0.f ? 0x80008000u : 0u;
 
-    bf16x8 qf[QH][2];
+    bf16x8 qf[2][2];
 #pragma unroll
-    for (int hq = 0; hq < QH; ++hq) {
-        const int q = qa + hq * 16 + (lane & 15);
+    for (int hq = 0; hq < 2; ++hq) {
+        const int q = qa + hq * 16 + li;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             u32x4 v = {0u, 0u, 0u, 0u};
@@ -362,170 +401,233 @@ __global__ __launch_bounds__(256, QH == 1 ? 4 : 2) void band_fused_kernel(BandGe
             qf[hq][kk] = __builtin_bit_cast(bf16x8, v);
         }
     }
-    const int span = kFT + 2 * w;
-    const int nblk = (span + kT - 1) / kT;
+    const int nblk = (kFT + 2 * w + kT - 1) / kT;
+    // this wave's key blocks: those that meet the band of one of its queries
+    const int lo = wv * kQW / kT;
+    const int hi = min(nblk - 1, (wv * kQW + kQW - 1 + 2 * w) / kT);
 
-    f32x4 o[QH][4], lsum[QH];
-#pragma unroll
-    for (int hq = 0; hq < QH; ++hq) {
-        lsum[hq] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int eb = 0; eb < 4; ++eb) o[hq][eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    }
-    float m_run[QH];
-#pragma unroll
-    for (int hq = 0; hq < QH; ++hq) m_run[hq] = -INFINITY;
-    const bf16x8 ones = __builtin_bit_cast(bf16x8, (u32x4){0x3f803f80u, 0x3f803f80u,
-                                                          0x3f803f80u, 0x3f803f80u});
-
-    // this thread's two 16-byte chunks of every K/V block: rows r0 and r0 + 32
-    const int r0 = threadIdx.x >> 3, ch = threadIdx.x & 7;
-    const int64_t row_step = (int64_t)kT * g.dil * kD;          // 64 subsequence rows
-    const int64_t half_step = (int64_t)32 * g.dil * kD;
-    int tt0 = t.q0 - w + r0;                                     // subsequence row of chunk 0
-    int64_t off0 = ((int64_t)t.b * g.l + t.rho) * kD + (int64_t)tt0 * g.dil * kD + ch * 8;
-    KVRegs r;
-    int blk0 = t.q0 - w;                                         // first key of the next block
-    auto gload = [&]() {
-        if (blk0 >= 0 && blk0 + kT <= t.lr) {                    // whole block in range
+    // DMA sources of this lane: key rows dr and dr + 32 of each block, chunk dch, as byte
+    // offsets from the start of the residue subsequence (uniform base pointers)
+    const int dr = wv * 8 + (lane >> 3);
+    const int dch = (lane & 7) ^ ((lane >> 3) & 7);
+    const int64_t seq0 = ((int64_t)t.b * g.l + t.rho) * kD;
+    const char* kseq = reinterpret_cast<const char*>(K + seq0);
+    const char* vseq = reinterpret_cast<const char*>(V + seq0);
+    const uint32_t row_bytes = (uint32_t)g.dil * kD * 2;
+    const char* zero = reinterpret_cast<const char*>(kBandZero);
+    int tt0 = t.q0 - w + dr;                         // key of row dr of block 0
+    uint32_t boff = (uint32_t)tt0 * row_bytes + dch * 16;   // used only when tt0 >= 0
+    auto dma = [&](int kb) {
+        u32x4* slot = lds + (kb % kSlots) * kSlotChunks;
+        const int tt = tt0 + kb * kT;
+        const uint32_t off = boff + (uint32_t)(kb * kT) * row_bytes;
+        if (t.q0 - w + kb * kT >= 0 && t.q0 - w + kb * kT + kT <= t.lr) {   // interior block
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                r.k[e] = *reinterpret_cast<const u32x4*>(K + off0 + e * half_step);
-                r.v[e] = *reinterpret_cast<const u32x4*>(V + off0 + e * half_step);
+                const uint32_t o2 = off + e * 32 * row_bytes;
+                __builtin_amdgcn_global_load_lds((const void*)(kseq + o2),
+                                                 (lds_void*)(slot + e * 256 + wv * 64), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((const void*)(vseq + o2),
+                                                 (lds_void*)(slot + 512 + e * 256 + wv * 64),
+                                                 16, 0, 0);
             }
         } else {
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                const int tt = tt0 + 32 * e;
-                u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-                if (tt >= 0 && tt < t.lr) {
-                    kv = *reinterpret_cast<const u32x4*>(K + off0 + e * half_step);
-                    vv = *reinterpret_cast<const u32x4*>(V + off0 + e * half_step);
-                }
-                r.k[e] = kv;
-                r.v[e] = vv;
+                const int te = tt + 32 * e;
+                const bool ok = te >= 0 && te < t.lr;
+                const uint32_t o2 = (uint32_t)te * row_bytes + dch * 16;
+                __builtin_amdgcn_global_load_lds((const void*)(ok ? kseq + o2 : zero),
+                                                 (lds_void*)(slot + e * 256 + wv * 64), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((const void*)(ok ? vseq + o2 : zero),
+                                                 (lds_void*)(slot + 512 + e * 256 + wv * 64),
+                                                 16, 0, 0);
             }
         }
-        tt0 += kT;
-        off0 += row_step;
-        blk0 += kT;
     };
-    gload();
-    lstore_block<true, true>(r, lk[0], lv[0]);
-    __syncthreads();
+    // LDS byte offsets (within a slot) of this lane's fragment reads
+    //   K fragment (ft, kk): key row 16ft + li, chunk 4kk + grp
+    //   V^T fragment (h, eb, i): key row 32h + 16i + 4grp + li/4, 8 bytes at column
+    //   16eb + 4(li%4), i.e. chunk 2eb + (li/2)%2, byte 8(li%2) of it
+    int koff[2], voff[4];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) koff[kk] = (li * 8 + ((4 * kk + grp) ^ (li & 7))) * 16;
+    {
+        const int vr = 4 * grp + (li >> 2);
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb)
+            voff[eb] = kT * 8 * 16 + (vr * 8 + ((2 * eb + ((li >> 1) & 1)) ^ (vr & 7))) * 16 +
+                       8 * (li & 1);
+    }
+    const char* lds_b = reinterpret_cast<const char*>(lds);
+    const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)lds;
+    // waits until at most `later` blocks (4 copies each per lane) are still in flight
+    auto wait_blocks = [](int later) {
+        static_assert(kSlots >= 3 && kSlots <= 6, "slot count");
+        if (later >= 3 && kSlots >= 6) wait_vmcnt<12>();
+        else if (later >= 2 && kSlots >= 5) wait_vmcnt<8>();
+        else if (later >= 1) wait_vmcnt<4>();
+        else wait_vmcnt<0>();
+    };
 
-    for (int kb = 0; kb < nblk; ++kb) {
-        const int cur = kb & 1;
-        const int t0 = t.q0 - w + kb * kT;
-        if (kb + 1 < nblk) gload();
-        const bool any = t0 + kT - 1 >= qa - w && t0 <= qa + kQPW - 1 + w;
-        if (any) {
-            // per query half: does the block meet its band, and is it entirely inside?
-            f32x4 s[QH][4];
-            const u32x4* lkc = lk[cur];
-            bf16x8 kf[4][2];          // all key fragments first, then the MFMAs
+    f32x4 o[2][4], lsum[2];
+    float m_run[2];
 #pragma unroll
-            for (int ft = 0; ft < 4; ++ft) {
-                const int row = ft * 16 + (lane & 15);
-                kf[ft][0] = __builtin_bit_cast(bf16x8, lkc[kswz(row, grp)]);
-                kf[ft][1] = __builtin_bit_cast(bf16x8, lkc[kswz(row, 4 + grp)]);
+    for (int hq = 0; hq < 2; ++hq) {
+        lsum[hq] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        m_run[hq] = -INFINITY;
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb) o[hq][eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, (u32x4){0x3f803f80u, 0x3f803f80u,
+                                                          0x3f803f80u, 0x3f803f80u});
+
+    auto read_k = [&](int kb, bf16x8 (&kf)[4][2]) {
+        const char* sb = lds_b + (kb % kSlots) * kSlotChunks * 16;
+#pragma unroll
+        for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk)
+                kf[ft][kk] = *reinterpret_cast<const bf16x8*>(sb + koff[kk] + ft * 16 * 128);
+    };
+    auto scores = [&](const bf16x8 (&kf)[4][2], f32x4 (&s)[2][4]) {
+#pragma unroll
+        for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+            for (int hq = 0; hq < 2; ++hq) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][0], qf[hq][0], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][1], qf[hq][1], acc, 0, 0, 0);
+                s[hq][ft] = acc;
             }
+    };
+
+    // One block iteration: softmax and P*V of block kb (scores in s) while the scores
+    // of block kb + 1 are computed into sn (at the wave's last block they are not used).
+    auto step = [&](int kb, f32x4 (&s)[2][4], f32x4 (&sn)[2][4]) {
+        const int t0 = t.q0 - w + kb * kT;
+        bf16x8 kf[4][2];
+        read_k(kb + 1, kf);
+        bool full = t0 >= qa + kQW - 1 - w && t0 + kT - 1 <= qa + w;
+        if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
+        if (!full) {                               // band (and range) mask, in place
 #pragma unroll
-            for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-                for (int hq = 0; hq < QH; ++hq) {
-                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][0], qf[hq][0], acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][1], qf[hq][1], acc, 0, 0, 0);
-                    s[hq][ft] = acc;
-                }
-            bf16x8 pf[QH][2];
-            // Softmax of one 16-query half: block max (4-lane reduction), lazy rescale,
-            // then p = exp2(score * scale * log2(e) - m) packed to bf16.  Full blocks and
-            // masked blocks run separate copies, so no mask arithmetic reaches full blocks.
-            auto soft = [&](int hq, auto masked) {
-                constexpr bool M = decltype(masked)::value;
-                const int q = qa + hq * 16 + (lane & 15);
-                float mb = -INFINITY;
+            for (int hq = 0; hq < 2; ++hq) {
+                const int base = t0 + 4 * grp - (qa + hq * 16 + li) + w;
 #pragma unroll
                 for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        if constexpr (M) {
+                        bool ok = (unsigned)(base + ft * 16 + v) <= (unsigned)(2 * w);
+                        if (MASK) {
                             const int tt = t0 + ft * 16 + 4 * grp + v;
-                            const int dj = tt - q;
-                            bool l = dj >= -w && dj <= w;
-                            if (MASK) l = l && tt >= 0 && tt < t.lr;
-                            if (!l) s[hq][ft][v] = -INFINITY;
+                            ok = ok && tt >= 0 && tt < t.lr;
                         }
-                        mb = fmaxf(mb, s[hq][ft][v]);
+                        s[hq][ft][v] = ok ? s[hq][ft][v] : -INFINITY;
                     }
-                mb = fmaxf(mb, __int_as_float(__builtin_amdgcn_ds_bpermute(xor16, __float_as_int(mb))));
-                mb = fmaxf(mb, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32, __float_as_int(mb))));
-                const float mbx = mb * sl2;               // block max in log2 units
-                const bool need = mbx > m_run[hq] + kLazy;
-                if (__any(need)) {
-                    const float m_new = need ? mbx : m_run[hq];
-                    const float corr = __builtin_amdgcn_exp2f(m_run[hq] - m_new);
-                    lsum[hq] *= corr;
-#pragma unroll
-                    for (int eb = 0; eb < 4; ++eb) o[hq][eb] *= corr;
-                    m_run[hq] = m_new;
-                }
-                const float nm = m_run[hq] == -INFINITY ? 0.f : -m_run[hq];
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    bf16x8 pv;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h][v], sl2, nm));
-                        float p1 =
-                            __builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h + 1][v], sl2, nm));
-                        if constexpr (M) {   // -inf * 0 (scale 0) must still give p = 0
-                            p0 = s[hq][2 * h][v] == -INFINITY ? 0.f : p0;
-                            p1 = s[hq][2 * h + 1][v] == -INFINITY ? 0.f : p1;
-                        }
-                        pv[v] = (__bf16)p0;
-                        pv[4 + v] = (__bf16)p1;
-                    }
-                    pf[hq][h] = pv;
-                }
-            };
-#pragma unroll
-            for (int hq = 0; hq < QH; ++hq) {
-                const int qh = qa + hq * 16;              // first query of this half
-                bool full = t0 - (qh + 15) >= -w && t0 + kT - 1 - qh <= w;
-                if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
-                if (full) soft(hq, std::false_type{});
-                else soft(hq, std::true_type{});
-            }
-            // O^T += V^T P^T and the denominator += 1^T P^T, over the block's keys
-            const int li = lane & 15;
-            const bf16_t* base = lv[cur] + (4 * grp + (li >> 2)) * kVLd + 4 * (li & 3);
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-#pragma unroll
-                for (int eb = 0; eb < 4; ++eb) {
-                    const bf16_t* p = base + 32 * h * kVLd + eb * 16;
-                    s16x4 both[2] = {tr_read(p), tr_read(p + 16 * kVLd)};
-                    const bf16x8 vf = __builtin_bit_cast(bf16x8, both);
-#pragma unroll
-                    for (int hq = 0; hq < QH; ++hq)
-                        o[hq][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[hq][h],
-                                                                            o[hq][eb], 0, 0, 0);
-                }
-#pragma unroll
-                for (int hq = 0; hq < QH; ++hq)
-                    lsum[hq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[hq][h],
-                                                                       lsum[hq], 0, 0, 0);
             }
         }
-        if (kb + 1 < nblk) lstore_block<true, true>(r, lk[cur ^ 1], lv[cur ^ 1]);
-        __syncthreads();
+        float mb[2];
+#pragma unroll
+        for (int hq = 0; hq < 2; ++hq) {
+            mb[hq] = -INFINITY;
+#pragma unroll
+            for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) mb[hq] = fmaxf(mb[hq], s[hq][ft][v]);
+        }
+        // lazy reference update; the row maximum (4 lanes) only when a lane asks for it
+        if (__any(mb[0] * sl2 > m_run[0] + kLazy || mb[1] * sl2 > m_run[1] + kLazy)) {
+#pragma unroll
+            for (int hq = 0; hq < 2; ++hq) {
+                float m = mb[hq];
+                m = fmaxf(m, __int_as_float(__builtin_amdgcn_ds_bpermute(xor16, __float_as_int(m))));
+                m = fmaxf(m, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32, __float_as_int(m))));
+                const float mbx = m * sl2;
+                const float m_new = mbx > m_run[hq] + kLazy ? mbx : m_run[hq];
+                const float corr =
+                    m_new == m_run[hq] ? 1.f : __builtin_amdgcn_exp2f(m_run[hq] - m_new);
+                lsum[hq] *= corr;
+#pragma unroll
+                for (int eb = 0; eb < 4; ++eb) o[hq][eb] *= corr;
+                m_run[hq] = m_new;
+            }
+        }
+        scores(kf, sn);
+        bf16x8 pf[2][2];
+#pragma unroll
+        for (int hq = 0; hq < 2; ++hq) {
+            const float nm = m_run[hq] == -INFINITY ? 0.f : -m_run[hq];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                bf16x8 pv;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    pv[v] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h][v], sl2, nm));
+                    pv[4 + v] =
+                        (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][2 * h + 1][v], sl2, nm));
+                }
+                pf[hq][h] = pv;
+            }
+        }
+        // P*V per 32-key half h: V^T fragments from key rows 32h and 32h + 16 of the slot
+        const uint32_t vb = lds_a + (kb % kSlots) * kSlotChunks * 16;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            bf16x8 vf[4];
+#pragma unroll
+            for (int eb = 0; eb < 4; ++eb) {
+                const uint32_t a = vb + voff[eb] + h * 32 * 128;
+                s16x4 r[2] = {tr_read_raw<0>(a), tr_read_raw<16 * 128>(a)};
+                vf[eb] = __builtin_bit_cast(bf16x8, r);
+            }
+            lds_wait(vf);
+#pragma unroll
+            for (int eb = 0; eb < 4; ++eb)
+#pragma unroll
+                for (int hq = 0; hq < 2; ++hq)
+                    o[hq][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[eb], pf[hq][h],
+                                                                        o[hq][eb], 0, 0, 0);
+#pragma unroll
+            for (int hq = 0; hq < 2; ++hq)
+                lsum[hq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[hq][h], lsum[hq],
+                                                                   0, 0, 0);
+        }
+    };
+    // One loop iteration over block kb: prefetch, compute (if the block meets the
+    // wave's band), then make block kb + 2 resident for the next iteration.
+    auto iter = [&](int kb, f32x4 (&s)[2][4], f32x4 (&sn)[2][4]) {
+        if (kb + kSlots - 1 < nblk) dma(kb + kSlots - 1);
+        if (kb >= lo && kb <= hi) {
+            if (kb == lo) {                        // the wave's first block
+                bf16x8 kf[4][2];
+                read_k(kb, kf);
+                scores(kf, s);
+            }
+            step(kb, s, sn);
+        }
+        // block kb + 2 is read by the next iteration: its copies must have landed; those
+        // of the blocks after it may still be in flight
+        wait_blocks(min(nblk - 1, kb + kSlots - 1) - (kb + 2));
+        block_sync();
+    };
+
+    // prologue: blocks 0 .. kSlots-2 in flight; blocks 0 and 1 resident before the loop
+#pragma unroll
+    for (int b = 0; b < kSlots - 1; ++b)
+        if (b < nblk) dma(b);
+    wait_blocks(min(nblk - 1, kSlots - 2) - 1);
+    block_sync();
+    // unrolled by two so the two score buffers alternate without register copies
+    f32x4 sa[2][4], sb[2][4];
+    for (int kb = 0; kb < nblk; kb += 2) {
+        iter(kb, sa, sb);
+        if (kb + 1 >= nblk) break;
+        iter(kb + 1, sb, sa);
     }
 #pragma unroll
-    for (int hq = 0; hq < QH; ++hq) {
-        const int q = qa + hq * 16 + (lane & 15);
+    for (int hq = 0; hq < 2; ++hq) {
+        const int q = qa + hq * 16 + li;
         if (q >= t.lr) continue;
         const float inv = 1.f / lsum[hq][0];
         OT* orow = O + row_off(g, t, q);
@@ -587,28 +689,19 @@ hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, voi
 
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
                              void* o, int o_bf16, int mask, hipStream_t stream) {
-    // OLLIE_BAND_QH (1 or 2) overrides the queries-per-wave choice, for tuning sweeps
-    static const int qh_env = [] {
-        const char* e = getenv("OLLIE_BAND_QH");
-        return e ? atoi(e) : 0;
-    }();
-    const int qh = qh_env == 2 ? 2 : 1;
     const int64_t l0 = (g.l + g.dil - 1) / g.dil;
-    const int ntx = (int)((l0 + 64 * qh - 1) / (64 * qh));
+    const int ntx = (int)((l0 + 127) / 128);
     const dim3 grid((unsigned)(ntx * g.dil * g.b));
-#define OLLIE_FUSED(OT, M, QH)                                                                \
-    hipLaunchKernelGGL((band_fused_kernel<OT, M, QH>), grid, dim3(256), 0, stream, g, ntx,     \
+#define OLLIE_FUSED(OT, M)                                                                   \
+    hipLaunchKernelGGL((band_fused_kernel<OT, M, 4>), grid, dim3(256), 0, stream, g, ntx,     \
                        (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
-#define OLLIE_FUSED_QH(OT, M) \
-    do { if (qh == 2) OLLIE_FUSED(OT, M, 2); else OLLIE_FUSED(OT, M, 1); } while (0)
     if (o_bf16) {
-        if (mask) OLLIE_FUSED_QH(bf16_t, true);
-        else OLLIE_FUSED_QH(bf16_t, false);
+        if (mask) OLLIE_FUSED(bf16_t, true);
+        else OLLIE_FUSED(bf16_t, false);
     } else {
-        if (mask) OLLIE_FUSED_QH(float, true);
-        else OLLIE_FUSED_QH(float, false);
+        if (mask) OLLIE_FUSED(float, true);
+        else OLLIE_FUSED(float, false);
     }
-#undef OLLIE_FUSED_QH
 #undef OLLIE_FUSED
     return hipGetLastError();
 }
