@@ -4,7 +4,7 @@ One step = one pass of the whole path over one batch of the four measured worklo
 through the public entry points, inputs already resident in HBM:
   derived_conv2d            ResNet conv3x3, N=16, C=K=256, 14x14            (GEMM + OffsetAdd)
   derived_conv_transpose2d  DCGAN convT 4x4 s2, N=16, 512->256, 8x8 -> 16x16 (GEMM + selective add)
-  derived_dilated_conv2d    CSRNet dilated conv3x3 d2, C=K=512, 96x128       (fused GEMM+OffsetAdd)
+  derived_dilated_conv2d    CSRNet dilated conv3x3 d2, C=K=512, 96x128       (GEMM + dilated OffsetAdd)
   banded_bmm                Longformer band, B=96, L=4096, d=64, w=256, dil 2 (fused G2BMM/softmax/GBMM)
 Each convolution runs the derived program variant that is faster for it (PATHS below);
 both variants are timed and reported.
@@ -39,7 +39,7 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 # derived-program variant per convolution workload: "staged" = GEMM stage + eOperator
 # through the Y scope, "fused" = the fused expression (no Y)
-PATHS = {2: "staged", 3: "staged", 4: "fused"}
+PATHS = {2: "fused", 3: "fused", 4: "fused"}
 
 
 def traffic_record(kernel_key):

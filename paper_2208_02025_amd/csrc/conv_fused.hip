@@ -47,22 +47,26 @@ struct FusedPlan {
     int tap_bh[kMaxTaps], tap_bw[kMaxTaps], tap_rs[kMaxTaps];
 };
 
-template <int BM, int BN, int NSTAGE, typename OT>
-__global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void conv_fused_kernel(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt, OT* __restrict__ out,
-    FusedPlan P) {
-    constexpr int WM = BM / 2, WN = BN / 2;
+// NW = 4 or 8 waves (2 x NW/2 over the tile).  Eight waves keep twice as many
+// global->LDS copies in flight per workgroup, which is what bounds the small shapes.
+template <int BM, int BN, int NSTAGE, typename OT, int NW = 4>
+__global__ __launch_bounds__(64 * NW, NSTAGE * (BM + BN) * kTileChunks * 16 <= 80 * 1024 ? 2 : 1)
+void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+                       OT* __restrict__ out, FusedPlan P) {
+    constexpr int NT = 64 * NW;
+    constexpr int WM = BM / 2, WN = BN / (NW / 2);
     constexpr int FM = WM / 16, FN = WN / 16;
     constexpr int STAGE_CHUNKS = (BM + BN) * kTileChunks;
-    constexpr int LOADS = STAGE_CHUNKS / 256;
-    constexpr int A_LOADS = BM * kTileChunks / 256;
-    static_assert(STAGE_CHUNKS % 256 == 0 && (BM * kTileChunks) % 256 == 0, "whole wave loads");
+    constexpr int LOADS = STAGE_CHUNKS / NT;
+    constexpr int A_LOADS = BM * kTileChunks / NT;
+    static_assert(STAGE_CHUNKS % NT == 0 && (BM * kTileChunks) % NT == 0, "whole wave loads");
+    static_assert(FM >= 1 && FN >= 1, "wave tile");
     __shared__ u32x4 lds[NSTAGE * STAGE_CHUNKS];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / (NW / 2), wn = wave % (NW / 2);
     const int nblk = gridDim.x;
     const int bid = blockIdx.x;
     const int id = (nblk & 7) == 0 ? (bid & 7) * (nblk >> 3) + (bid >> 3) : bid;
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void conv_fused_kernel(
     bool rowok[A_LOADS];
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
-        const int row = (i * 4 + wave) * 8 + (lane >> 3);
+        const int row = (i * NW + wave) * 8 + (lane >> 3);
         const int m = m0 + row;
         rowok[i] = m < mc;
         const int mm = m < mc ? m : 0;
@@ -104,7 +108,7 @@ __global__ __launch_bounds__(256, NSTAGE == 2 ? 2 : 1) void conv_fused_kernel(
         const int buf = it % NSTAGE;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
-            const int seg = i * 4 + wave;
+            const int seg = i * NW + wave;
             const int row = seg * 8 + (lane >> 3);
             const int ch = (lane & 7) ^ (row & 7);
             const bf16_t* p;
@@ -250,17 +254,17 @@ int64_t plan_tiles(FusedPlan& P, int bm, int bn) {
     return t;
 }
 
-template <int BM, int BN, int NS, typename OT>
+template <int BM, int BN, int NS, typename OT, int NW = 4>
 hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, hipStream_t st) {
     const int64_t tiles = plan_tiles(P, BM, BN);
     if (tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL((conv_fused_kernel<BM, BN, NS, OT>), dim3((unsigned)tiles), dim3(256), 0,
+    hipLaunchKernelGGL((conv_fused_kernel<BM, BN, NS, OT, NW>), dim3((unsigned)tiles), dim3(64 * NW), 0,
                        st, (const bf16_t*)x, (const bf16_t*)wt, (OT*)out, P);
     return hipGetLastError();
 }
 
-// 0 = 128x128 (two workgroups per CU), 1 = 64x128, 2 = 64x64; OLLIE_FUSED_CONFIG
-// overrides the shape-based choice for tuning sweeps.
+// 0 = 128x128 with 8 waves (two workgroups per CU), 1 = 64x128 with 4 waves, 2 = 64x64
+// with 8 waves; OLLIE_FUSED_CONFIG overrides the shape-based choice for tuning sweeps.
 template <typename OT>
 hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, hipStream_t st) {
     static const int forced = [] {
@@ -275,9 +279,9 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, hipS
         else cfg = 2;
     }
     switch (cfg) {
-    case 0: return go<128, 128, 2, OT>(P, x, wt, out, st);
-    case 1: return go<64, 128, 2, OT>(P, x, wt, out, st);
-    default: return go<64, 64, 2, OT>(P, x, wt, out, st);
+    case 0: return go<128, 128, 2, OT, 8>(P, x, wt, out, st);
+    case 1: return go<64, 128, 2, OT, 4>(P, x, wt, out, st);
+    default: return go<64, 64, 2, OT, 8>(P, x, wt, out, st);
     }
 }
 
