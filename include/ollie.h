@@ -29,7 +29,8 @@
  *
  * Common buffer rules: tensors are dense and row-major in the layouts stated below;
  * pointers must be 16-byte aligned (else OLLIE_EALIGN); outputs must not alias
- * inputs or the workspace.
+ * inputs or the workspace (one stated exception: a fused residual, see
+ * ollie_conv_epilogue).
  */
 #ifndef OLLIE_H
 #define OLLIE_H
@@ -86,6 +87,26 @@ typedef struct {
     int32_t in_dtype;      /* ollie_dtype */
     int32_t out_dtype;     /* ollie_dtype */
 } ollie_conv_desc;
+
+/* Element-wise tail of a convolution-family operator, evaluated inside its eOperator
+ * (or inside the fused expression) right before the store -- the fusion of OffsetAdd
+ * with the element-wise operators that follow it (section 6.3):
+ *   out[n][ho][wo][k] = act( conv[n][ho][wo][k] + bias[k] + residual[n][ho][wo][k] )
+ * with act = ReLU (max(., 0)) when relu != 0, the identity otherwise.  conv is the
+ * operator's fp32 accumulation; the additions and the ReLU run in fp32 in this order,
+ * then the result is converted to out_dtype.
+ *   bias      [k] in bias_dtype, or NULL (no bias term)
+ *   residual  [n][ho][wo][k] (the layout of out) in residual_dtype, or NULL; it may be
+ *             the same buffer as out (each element is read before it is overwritten,
+ *             by the same thread), but may not overlap it otherwise.
+ * Both pointers must be 16-byte aligned; dtypes are OLLIE_F32 or OLLIE_BF16. */
+typedef struct {
+    const void* bias;
+    const void* residual;
+    int32_t bias_dtype;      /* ollie_dtype */
+    int32_t residual_dtype;  /* ollie_dtype */
+    int32_t relu;            /* 0 or 1 */
+} ollie_conv_epilogue;
 
 /* Geometry of banded_bmm.
  *   Q, K, V [b][l][d] bf16, O [b][l][d] (out_dtype F32 or BF16).
@@ -168,6 +189,21 @@ int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const voi
 int derived_conv_transpose2d(const ollie_conv_desc* desc, const void* x, const void* wt,
                              void* out, void* ws, size_t ws_bytes, uint32_t flags,
                              void* stream);
+
+/* The three operators above with an element-wise tail (ollie_conv_epilogue) fused
+ * into their last kernel, for both the two-stage and the fused path.  epi == NULL is
+ * the plain operator.  Extra checks: relu not in {0, 1} or a bias/residual pointer
+ * that is not 16-byte aligned -> OLLIE_EINVAL / OLLIE_EALIGN; an unknown
+ * bias_dtype/residual_dtype of a non-NULL tensor -> OLLIE_EDTYPE. */
+int derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
+                      void* ws, size_t ws_bytes, uint32_t flags,
+                      const ollie_conv_epilogue* epi, void* stream);
+int derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+                              void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                              const ollie_conv_epilogue* epi, void* stream);
+int derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+                                void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                                const ollie_conv_epilogue* epi, void* stream);
 
 /* Banded dilated batched matmul with row softmax (Longformer-style sliding window):
  *   S[b][i][j] = scale * sum_e Q[b][i][e] * K0[b][t][e],  t = i + (j-w)*dilation

@@ -127,6 +127,22 @@ def conv_transpose2d(x, wt, stride=1, pad=0, dil=1, out_pad=0, idx=None):
     return _conv(x, wt, stride, pad, dil, out_pad, True, idx)
 
 
+def conv_epilogue(conv, bias=None, residual=None, relu=False):
+    """Element-wise tail of a convolution (section 6.3: OffsetAdd fused with the
+    element-wise operators after it), by its definition in float64:
+        out[n][ho][wo][k] = act(conv[n][ho][wo][k] + bias[k] + residual[n][ho][wo][k])
+    with act = max(., 0) when relu, the identity otherwise.  conv is the operator's
+    output [N, HO, WO, K]; bias [K] and residual [N, HO, WO, K] are optional."""
+    y = np.asarray(conv, dtype=np.float64).copy()
+    if bias is not None:
+        y = y + _f32(bias).astype(np.float64).reshape(1, 1, 1, -1)
+    if residual is not None:
+        y = y + _f32(residual).astype(np.float64)
+    if relu:
+        y = np.where(y < 0.0, 0.0, y)
+    return y
+
+
 def band(q, k, v, w, dil, scale=1.0, mask=False, rows=None, want_s=True, want_p=True):
     """Banded dilated batched matmul + row softmax + band-times-dense product.
 

@@ -31,6 +31,7 @@ _STATUS_NAMES = {OK: "OLLIE_OK", EINVAL: "OLLIE_EINVAL", EDTYPE: "OLLIE_EDTYPE",
                  EWORKSPACE: "OLLIE_EWORKSPACE", EALIGN: "OLLIE_EALIGN", EHIP: "OLLIE_EHIP"}
 
 EXPORTS = ("derived_conv2d", "derived_dilated_conv2d", "derived_conv_transpose2d", "banded_bmm",
+           "derived_conv2d_ex", "derived_dilated_conv2d_ex", "derived_conv_transpose2d_ex",
            "ollie_conv_out_hw", "ollie_conv_workspace_bytes", "ollie_band_workspace_bytes",
            "ollie_last_error", "ollie_version", "ollie_gemm_nt", "ollie_eop_gather",
            "ollie_band_g2bmm", "ollie_band_softmax", "ollie_band_gbmm")
@@ -45,6 +46,12 @@ class ConvDesc(ctypes.Structure):
                 ("dil_h", ctypes.c_int32), ("dil_w", ctypes.c_int32),
                 ("out_pad_h", ctypes.c_int32), ("out_pad_w", ctypes.c_int32),
                 ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class ConvEpilogue(ctypes.Structure):
+    _fields_ = [("bias", ctypes.c_void_p), ("residual", ctypes.c_void_p),
+                ("bias_dtype", ctypes.c_int32), ("residual_dtype", ctypes.c_int32),
+                ("relu", ctypes.c_int32)]
 
 
 class BandDesc(ctypes.Structure):
@@ -74,10 +81,14 @@ def load_library(path: str = LIB_PATH):
     p, i64, i32, u32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32,
                             ctypes.c_size_t)
     cdp, bdp = ctypes.POINTER(ConvDesc), ctypes.POINTER(BandDesc)
+    edp = ctypes.POINTER(ConvEpilogue)
     sig = {
         "derived_conv2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
         "derived_dilated_conv2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
         "derived_conv_transpose2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
+        "derived_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
+        "derived_dilated_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
+        "derived_conv_transpose2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
         "banded_bmm": ([bdp, p, p, p, p, p, p, sz, u32, p], ctypes.c_int),
         "ollie_conv_out_hw": ([cdp, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64)],
                               ctypes.c_int),
@@ -160,8 +171,22 @@ def conv_workspace_bytes(desc: ConvDesc, transposed: bool, flags: int = 0) -> in
                                                          flags))
 
 
+def conv_epilogue(bias=None, residual=None, relu=False):
+    """The element-wise tail act(conv + bias[k] + residual) as the library's struct, or
+    None when there is no term (bias [K], residual shaped like out, fp32 or bf16)."""
+    if bias is None and residual is None and not relu:
+        return None
+    for t, name in ((bias, "bias"), (residual, "residual")):
+        if t is not None:
+            _gpu(t, name)
+    return ConvEpilogue(None if bias is None else bias.data_ptr(),
+                        None if residual is None else residual.data_ptr(),
+                        F32 if bias is None else _dtype_code(bias.dtype),
+                        F32 if residual is None else _dtype_code(residual.dtype), int(bool(relu)))
+
+
 def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output_padding,
-          out_dtype, y_bf16, out, ws, fuse=False):
+          out_dtype, y_bf16, out, ws, fuse=False, bias=None, residual=None, relu=False):
     _gpu(x, "x")
     _gpu(wt, "wt")
     if x.dtype != wt.dtype:
@@ -180,34 +205,47 @@ def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output
     if ws is None and need:
         ws = torch.empty(need, dtype=torch.uint8, device=x.device)
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
-    st = getattr(load_library(), entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out),
-                                        _ptr(ws), ws_bytes, flags, _stream(x.device))
+    epi = conv_epilogue(bias, residual, relu)
+    if bias is not None and tuple(bias.shape) != (desc.k,):
+        raise ValueError(f"bias must have shape ({desc.k},)")
+    if residual is not None and tuple(residual.shape) != (desc.n, ho, wo, desc.k):
+        raise ValueError("residual must have the shape of out")
+    lib = load_library()
+    if epi is None:
+        st = getattr(lib, entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out), _ptr(ws),
+                                 ws_bytes, flags, _stream(x.device))
+    else:
+        entry = entry + "_ex"
+        st = getattr(lib, entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out), _ptr(ws),
+                                 ws_bytes, flags, ctypes.byref(epi), _stream(x.device))
     _check(st, entry)
     return out
 
 
 def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=False,
-                   out=None, ws=None, fuse=False):
+                   out=None, ws=None, fuse=False, bias=None, residual=None, relu=False):
     """Conv2d (dilation 1) as GEMM + OffsetAdd eOperator (fuse=True: the fused
-    expression, no Y).  x [N,H,W,C], wt [R,S,K,C]."""
+    expression, no Y).  x [N,H,W,C], wt [R,S,K,C].  bias / residual / relu: an
+    element-wise tail act(conv + bias + residual) evaluated in the last kernel."""
     return _conv("derived_conv2d", False, x, wt, stride, padding, 1, 0, out_dtype, y_bf16,
-                 out, ws, fuse)
+                 out, ws, fuse, bias, residual, relu)
 
 
 def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,
-                           y_bf16=False, out=None, ws=None, fuse=False):
+                           y_bf16=False, out=None, ws=None, fuse=False, bias=None,
+                           residual=None, relu=False):
     """Dilated Conv2d as GEMM + dilated OffsetAdd eOperator."""
     return _conv("derived_dilated_conv2d", False, x, wt, stride, padding, dilation, 0,
-                 out_dtype, y_bf16, out, ws, fuse)
+                 out_dtype, y_bf16, out, ws, fuse, bias, residual, relu)
 
 
 def derived_conv_transpose2d(x, wt, stride=1, padding=0, output_padding=0, dilation=1,
                              out_dtype=torch.float32, y_bf16=False, out=None, ws=None,
-                             fuse=False):
+                             fuse=False, bias=None, residual=None, relu=False):
     """ConvTranspose2d as GEMM on the unpadded input + selective-add eOperator.
     x [N,H,W,C_in], wt [R,S,C_out,C_in]."""
     return _conv("derived_conv_transpose2d", True, x, wt, stride, padding, dilation,
-                 output_padding, out_dtype, y_bf16, out, ws, fuse)
+                 output_padding, out_dtype, y_bf16, out, ws, fuse, bias, residual, relu)
 
 
 def band_desc(q_shape, w, dilation, scale=1.0, out_dtype=torch.float32) -> BandDesc:

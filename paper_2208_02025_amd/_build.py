@@ -19,8 +19,9 @@ SOURCES = ["abi.hip", "gemm.hip", "eop.hip", "band.hip", "conv_fused.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 ops are disabled for all device code (the host pass warns that it does
-# not know the feature; that is harmless).
-HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+# not know the feature; that is harmless).  Symbols are hidden by default; abi.hip
+# exports exactly the functions include/ollie.h declares.
+HIPCC_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", f"--offload-arch={ARCH}",
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                "-Wall", "-Wno-unused-function"]
 

@@ -121,10 +121,28 @@ int check_gemm(int64_t m, int64_t n, int64_t k, const void* a, const void* b, co
     return OLLIE_OK;
 }
 
+// Validates an optional element-wise tail and converts it to the kernels' form.
+int make_epi(const ollie_conv_epilogue* e, Epi* out) {
+    *out = Epi{nullptr, nullptr, 0, 0, 0};
+    if (!e) return OLLIE_OK;
+    if (e->relu != 0 && e->relu != 1) return fail(OLLIE_EINVAL, "epilogue relu must be 0 or 1");
+    if ((e->bias && !dtype_ok(e->bias_dtype)) || (e->residual && !dtype_ok(e->residual_dtype)))
+        return fail(OLLIE_EDTYPE, "epilogue bias/residual dtype must be OLLIE_F32 or OLLIE_BF16");
+    if (!aligned16(e->bias) || !aligned16(e->residual))
+        return fail(OLLIE_EALIGN, "epilogue bias/residual pointers must be 16-byte aligned");
+    *out = Epi{e->bias, e->residual, e->bias_dtype == OLLIE_BF16,
+               e->residual_dtype == OLLIE_BF16, e->relu};
+    return OLLIE_OK;
+}
+
 int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
-                void* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+                void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                const ollie_conv_epilogue* epilogue, void* stream) {
     int64_t ho, wo;
     int st = check_conv_geom(d, transposed, &ho, &wo);
+    if (st) return st;
+    Epi epi;
+    st = make_epi(epilogue, &epi);
     if (st) return st;
     if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE))
         return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
@@ -135,7 +153,7 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
         if (!aligned16(x) || !aligned16(wt) || !aligned16(out))
             return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
         hipError_t e = launch_conv_fused(conv_geom(d, ho, wo), transposed, x, wt, out,
-                                         d->out_dtype == OLLIE_BF16, (hipStream_t)stream);
+                                         d->out_dtype == OLLIE_BF16, epi, (hipStream_t)stream);
         if (e != hipSuccess) return hip_fail(e, "fused GEMM+eOperator launch");
         return OLLIE_OK;
     }
@@ -155,7 +173,7 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     hipError_t e = launch_gemm_nt(m, nc, d->c, x, wt, ws, d->in_dtype == OLLIE_BF16, y_bf16, s);
     if (e != hipSuccess) return hip_fail(e, "GEMM stage launch");
     e = launch_eop_gather(conv_geom(d, ho, wo), transposed, ws, y_bf16, out,
-                          d->out_dtype == OLLIE_BF16, s);
+                          d->out_dtype == OLLIE_BF16, epi, s);
     if (e != hipSuccess) return hip_fail(e, "eOperator launch");
     return OLLIE_OK;
 }
@@ -198,6 +216,7 @@ constexpr int64_t kSoftmaxMaxBand = 16 * 64;   // register-resident row length o
 
 }  // namespace
 
+#pragma GCC visibility push(default)
 extern "C" {
 
 const char* ollie_last_error(void) { return g_err; }
@@ -222,25 +241,43 @@ size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags) {
     return band_p_offset(desc) + band_p_bytes(desc);
 }
 
-int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
-                   void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+int derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
+                      void* ws, size_t ws_bytes, uint32_t flags,
+                      const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
     if (desc && (desc->dil_h != 1 || desc->dil_w != 1))
         return fail(OLLIE_EINVAL, "derived_conv2d takes dilation 1; use derived_dilated_conv2d");
-    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, stream);
+    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
+}
+
+int derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+                              void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                              const ollie_conv_epilogue* epi, void* stream) {
+    g_err[0] = 0;
+    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
+}
+
+int derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+                                void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                                const ollie_conv_epilogue* epi, void* stream) {
+    g_err[0] = 0;
+    return conv_common(desc, 1, x, wt, out, ws, ws_bytes, flags, epi, stream);
+}
+
+int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
+                   void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
+    return derived_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
 }
 
 int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt,
                            void* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
-    g_err[0] = 0;
-    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, stream);
+    return derived_dilated_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
 }
 
 int derived_conv_transpose2d(const ollie_conv_desc* desc, const void* x, const void* wt,
                              void* out, void* ws, size_t ws_bytes, uint32_t flags,
                              void* stream) {
-    g_err[0] = 0;
-    return conv_common(desc, 1, x, wt, out, ws, ws_bytes, flags, stream);
+    return derived_conv_transpose2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
 }
 
 int banded_bmm(const ollie_band_desc* desc, const void* q, const void* k, const void* v,
@@ -306,7 +343,7 @@ int ollie_eop_gather(const ollie_conv_desc* desc, int transposed, const void* y,
         return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
     hipError_t e = launch_eop_gather(conv_geom(desc, ho, wo), transposed ? 1 : 0, y,
                                      y_dtype == OLLIE_BF16, out, desc->out_dtype == OLLIE_BF16,
-                                     (hipStream_t)stream);
+                                     Epi{nullptr, nullptr, 0, 0, 0}, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "eOperator launch");
     return OLLIE_OK;
 }
@@ -358,3 +395,4 @@ int ollie_band_gbmm(const ollie_band_desc* desc, const void* p, const void* v, v
 }
 
 }  // extern "C"
+#pragma GCC visibility pop

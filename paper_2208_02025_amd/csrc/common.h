@@ -62,6 +62,39 @@ template <> struct In<bf16_t> {
     }
 };
 
+// Element-wise tail of a convolution-family operator: + bias[k] + residual[pixel][k],
+// then ReLU, in fp32 right before the store (a null pointer drops its term).
+struct Epi {
+    const void* bias;
+    const void* res;
+    int bias_bf16, res_bf16, relu;
+};
+__device__ __forceinline__ float epi_load(const void* p, int bf16, int64_t i) {
+    return bf16 ? bf2f(reinterpret_cast<const bf16_t*>(p)[i])
+                : reinterpret_cast<const float*>(p)[i];
+}
+__device__ __forceinline__ f32x4 epi_load4(const void* p, int bf16, int64_t i) {
+    return bf16 ? In<bf16_t>::get4(reinterpret_cast<const bf16_t*>(p) + i)
+                : In<float>::get4(reinterpret_cast<const float*>(p) + i);
+}
+// ReLU that keeps a NaN a NaN (x < 0 is false for NaN)
+__device__ __forceinline__ float relu_f(float x) { return x < 0.f ? 0.f : x; }
+// v = out[oi + j] for channels k + j, j = 0..3 (oi, k multiples of 4)
+__device__ __forceinline__ f32x4 epi_apply4(const Epi& e, f32x4 v, int64_t oi, int64_t k) {
+    if (e.bias) v += epi_load4(e.bias, e.bias_bf16, k);
+    if (e.res) v += epi_load4(e.res, e.res_bf16, oi);
+    if (e.relu) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = relu_f(v[j]);
+    }
+    return v;
+}
+__device__ __forceinline__ float epi_apply(const Epi& e, float v, int64_t oi, int64_t k) {
+    if (e.bias) v += epi_load(e.bias, e.bias_bf16, k);
+    if (e.res) v += epi_load(e.res, e.res_bf16, oi);
+    return e.relu ? relu_f(v) : v;
+}
+
 // ------------------------------------------------- shared GEMM-tile building blocks
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -103,13 +136,13 @@ struct ConvGeom {
 };
 
 hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, int y_bf16,
-                             void* out, int out_bf16, hipStream_t stream);
+                             void* out, int out_bf16, const Epi& epi, hipStream_t stream);
 
 // Fused GEMM + eOperator (output-stationary), bf16 operands.  Returns
 // hipErrorInvalidValue when the shape is outside what the fused kernel supports.
 bool conv_fused_supported(const ConvGeom& g, int transposed);
 hipError_t launch_conv_fused(const ConvGeom& g, int transposed, const void* x, const void* wt,
-                             void* out, int out_bf16, hipStream_t stream);
+                             void* out, int out_bf16, const Epi& epi, hipStream_t stream);
 
 struct BandGeom {
     int64_t b, l, d, w;

@@ -7,7 +7,8 @@
 // i.e. one contraction over (tap, c) whose A operand is X gathered through the
 // eOperator's index map.  This kernel evaluates that fused expression output-stationary:
 // a tile of output pixels x output channels accumulates over taps and channel blocks in
-// MFMA registers, so Y never exists, not even on chip.
+// MFMA registers, so Y never exists, not even on chip.  An element-wise tail (bias,
+// residual, ReLU) is applied to the accumulators before the store.
 //
 // Output pixels are grouped into classes that share their tap list:
 //   forward conv:     one class; input row hi = stride*ho - pad + r*dil (per-pixel
@@ -52,7 +53,7 @@ struct FusedPlan {
 template <int BM, int BN, int NSTAGE, typename OT, int NW = 4>
 __global__ __launch_bounds__(64 * NW, NSTAGE * (BM + BN) * kTileChunks * 16 <= 80 * 1024 ? 2 : 1)
 void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
-                       OT* __restrict__ out, FusedPlan P) {
+                       OT* __restrict__ out, FusedPlan P, Epi epi) {
     constexpr int NT = 64 * NW;
     constexpr int WM = BM / 2, WN = BN / (NW / 2);
     constexpr int FM = WM / 16, FN = WN / 16;
@@ -180,11 +181,13 @@ void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ 
         for (int i = 0; i < FN; ++i) {
             const int k = k0 + wn * WN + i * 16 + 4 * (lane >> 4);
             if (vec_ok && k + 3 < K) {
-                Out<OT>::put4(orow + k, acc[i][j]);
+                Out<OT>::put4(orow + k, epi_apply4(epi, acc[i][j], opix * K + k, k));
             } else {
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    if (k + v < K) Out<OT>::put(orow + k + v, acc[i][j][v]);
+                    if (k + v < K)
+                        Out<OT>::put(orow + k + v,
+                                     epi_apply(epi, acc[i][j][v], opix * K + k + v, k + v));
             }
         }
     }
@@ -255,18 +258,20 @@ int64_t plan_tiles(FusedPlan& P, int bm, int bn) {
 }
 
 template <int BM, int BN, int NS, typename OT, int NW = 4>
-hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, hipStream_t st) {
+hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
+              hipStream_t st) {
     const int64_t tiles = plan_tiles(P, BM, BN);
     if (tiles == 0) return hipSuccess;
     hipLaunchKernelGGL((conv_fused_kernel<BM, BN, NS, OT, NW>), dim3((unsigned)tiles), dim3(64 * NW), 0,
-                       st, (const bf16_t*)x, (const bf16_t*)wt, (OT*)out, P);
+                       st, (const bf16_t*)x, (const bf16_t*)wt, (OT*)out, P, epi);
     return hipGetLastError();
 }
 
 // 0 = 128x128 with 8 waves (two workgroups per CU), 1 = 64x128 with 4 waves, 2 = 64x64
 // with 8 waves; OLLIE_FUSED_CONFIG overrides the shape-based choice for tuning sweeps.
 template <typename OT>
-hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, hipStream_t st) {
+hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
+                    hipStream_t st) {
     static const int forced = [] {
         const char* e = getenv("OLLIE_FUSED_CONFIG");
         return e ? atoi(e) : -1;
@@ -279,9 +284,9 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, hipS
         else cfg = 2;
     }
     switch (cfg) {
-    case 0: return go<128, 128, 2, OT, 8>(P, x, wt, out, st);
-    case 1: return go<64, 128, 2, OT, 4>(P, x, wt, out, st);
-    default: return go<64, 64, 2, OT, 8>(P, x, wt, out, st);
+    case 0: return go<128, 128, 2, OT, 8>(P, x, wt, out, epi, st);
+    case 1: return go<64, 128, 2, OT, 4>(P, x, wt, out, epi, st);
+    default: return go<64, 64, 2, OT, 8>(P, x, wt, out, epi, st);
     }
 }
 
@@ -294,11 +299,11 @@ bool conv_fused_supported(const ConvGeom& g, int transposed) {
 }
 
 hipError_t launch_conv_fused(const ConvGeom& g, int transposed, const void* x, const void* wt,
-                             void* out, int out_bf16, hipStream_t stream) {
+                             void* out, int out_bf16, const Epi& epi, hipStream_t stream) {
     FusedPlan P;
     if (g.c % kTileK != 0 || !make_plan(g, transposed, P)) return hipErrorInvalidValue;
-    return out_bf16 ? dispatch<bf16_t>(P, x, wt, out, stream)
-                    : dispatch<float>(P, x, wt, out, stream);
+    return out_bf16 ? dispatch<bf16_t>(P, x, wt, out, epi, stream)
+                    : dispatch<float>(P, x, wt, out, epi, stream);
 }
 
 }  // namespace ollie

@@ -8,7 +8,9 @@
 //     th = ho + ph - r*dh >= 0, th % sh == 0, hi = th / sh < h  (likewise along w)
 //
 // Taps outside the image are never read (boundary tightening, section 4.2), so each
-// element of Y is read at most once.  One thread owns VEC consecutive output channels
+// element of Y is read at most once.  An element-wise tail (bias, residual, ReLU) is
+// applied to the sum before the store: OffsetAdd fused with the element-wise operators
+// that follow it (section 6.3).  One thread owns VEC consecutive output channels
 // of one output pixel; a wavefront covers 64*VEC contiguous channels, so every tap
 // is one contiguous, coalesced read of a K-vector.
 #include "common.h"
@@ -20,7 +22,7 @@ namespace {
 template <typename YT, typename OT, int VEC, bool TRANSPOSED>
 __global__ __launch_bounds__(256) void eop_gather_kernel(const YT* __restrict__ Y,
                                                          OT* __restrict__ out, ConvGeom g,
-                                                         int64_t total) {
+                                                         int64_t total, Epi epi) {
     const int64_t item = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (item >= total) return;
     const int kv = (int)(g.k / VEC);
@@ -74,46 +76,49 @@ __global__ __launch_bounds__(256) void eop_gather_kernel(const YT* __restrict__ 
             }
         }
     }
-    OT* dst = out + (((int64_t)n * ho_n + ho) * wo_n + wo) * K + k;
+    const int64_t oi = (((int64_t)n * ho_n + ho) * wo_n + wo) * K + k;
+    OT* dst = out + oi;
     if (VEC == 4) {
         f32x4 v = {acc[0], acc[1], acc[2], acc[3]};
-        Out<OT>::put4(dst, v);
+        Out<OT>::put4(dst, epi_apply4(epi, v, oi, k));
     } else {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) Out<OT>::put(dst + e, acc[e]);
+        for (int e = 0; e < VEC; ++e)
+            Out<OT>::put(dst + e, epi_apply(epi, acc[e], oi + e, k + e));
     }
 }
 
 template <typename YT, typename OT, int VEC>
-hipError_t go(const ConvGeom& g, int transposed, const void* y, void* out, hipStream_t st) {
+hipError_t go(const ConvGeom& g, int transposed, const void* y, void* out, const Epi& epi,
+              hipStream_t st) {
     int64_t total = g.n * g.ho * g.wo * (g.k / VEC);
     if (total == 0) return hipSuccess;
     dim3 grid((unsigned)((total + 255) / 256));
     if (transposed)
         hipLaunchKernelGGL((eop_gather_kernel<YT, OT, VEC, true>), grid, dim3(256), 0, st,
-                           (const YT*)y, (OT*)out, g, total);
+                           (const YT*)y, (OT*)out, g, total, epi);
     else
         hipLaunchKernelGGL((eop_gather_kernel<YT, OT, VEC, false>), grid, dim3(256), 0, st,
-                           (const YT*)y, (OT*)out, g, total);
+                           (const YT*)y, (OT*)out, g, total, epi);
     return hipGetLastError();
 }
 
 template <typename YT, typename OT>
 hipError_t pick_vec(const ConvGeom& g, int transposed, const void* y, void* out,
-                    hipStream_t st) {
-    if ((g.k & 3) == 0) return go<YT, OT, 4>(g, transposed, y, out, st);
-    return go<YT, OT, 1>(g, transposed, y, out, st);
+                    const Epi& epi, hipStream_t st) {
+    if ((g.k & 3) == 0) return go<YT, OT, 4>(g, transposed, y, out, epi, st);
+    return go<YT, OT, 1>(g, transposed, y, out, epi, st);
 }
 
 }  // namespace
 
 hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, int y_bf16,
-                             void* out, int out_bf16, hipStream_t stream) {
+                             void* out, int out_bf16, const Epi& epi, hipStream_t stream) {
     if (y_bf16)
-        return out_bf16 ? pick_vec<bf16_t, bf16_t>(g, transposed, y, out, stream)
-                        : pick_vec<bf16_t, float>(g, transposed, y, out, stream);
-    return out_bf16 ? pick_vec<float, bf16_t>(g, transposed, y, out, stream)
-                    : pick_vec<float, float>(g, transposed, y, out, stream);
+        return out_bf16 ? pick_vec<bf16_t, bf16_t>(g, transposed, y, out, epi, stream)
+                        : pick_vec<bf16_t, float>(g, transposed, y, out, epi, stream);
+    return out_bf16 ? pick_vec<float, bf16_t>(g, transposed, y, out, epi, stream)
+                    : pick_vec<float, float>(g, transposed, y, out, epi, stream);
 }
 
 }  // namespace ollie

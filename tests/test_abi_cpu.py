@@ -199,3 +199,44 @@ def test_fused_workspace_sizes(lib):
     assert ol.conv_workspace_bytes(d, False, ol.FUSE_EPILOGUE) > 0
     d = conv(n=16, c=512, h=8, w=8, k=256, r=4, s=4, stride=2, pad=1)
     assert ol.conv_workspace_bytes(d, True, ol.FUSE_EPILOGUE) == 0
+
+
+def test_epilogue_error_paths(lib):
+    d = conv()
+    def call(entry, **kw):
+        e = ol.ConvEpilogue(kw.get("bias", W16.value), kw.get("residual", None),
+                            kw.get("bias_dtype", ol.F32), kw.get("residual_dtype", ol.F32),
+                            kw.get("relu", 1))
+        st = getattr(lib, entry)(ctypes.byref(d), A16, B16, C16, W16, 1 << 40, 0,
+                                 ctypes.byref(e), None)
+        return st, lib.ollie_last_error().decode()
+    for entry in ("derived_conv2d_ex", "derived_dilated_conv2d_ex"):
+        assert call(entry, relu=2)[0] == ol.EINVAL
+        assert call(entry, bias_dtype=7)[0] == ol.EDTYPE
+        assert call(entry, residual=C16.value, residual_dtype=5)[0] == ol.EDTYPE
+        assert call(entry, bias=0x40008)[0] == ol.EALIGN
+        assert call(entry, residual=0x40004)[0] == ol.EALIGN
+        st, msg = call(entry, relu=3)
+        assert msg
+    # a NULL tensor's dtype is not looked at
+    dt = conv(stride=2)
+    e = ol.ConvEpilogue(None, None, 9, 9, 0)
+    st = lib.derived_conv_transpose2d_ex(ctypes.byref(dt), A16, B16, C16, W16, 10, 0,
+                                         ctypes.byref(e), None)
+    assert st == ol.EWORKSPACE          # the epilogue passed; the workspace check fired
+    # the plain entry points are the _ex ones with no tail
+    st = lib.derived_conv2d_ex(ctypes.byref(conv(dil=2, pad=2)), A16, B16, C16, W16, 1 << 40,
+                               0, None, None)
+    assert st == ol.EINVAL
+
+
+def test_library_exports_nothing_else(lib):
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    res = subprocess.run([nm, "-D", "--defined-only", ol.LIB_PATH], capture_output=True,
+                         text=True, check=True)
+    funcs = {ln.split()[-1] for ln in res.stdout.splitlines() if " T " in ln}
+    assert funcs == set(header_functions())

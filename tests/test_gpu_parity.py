@@ -515,3 +515,104 @@ def test_hip_graph_replays_match_eager():
         assert float(junk.abs().sum()) >= 0
         for got, exp in zip((o2, o4, ob), ref):
             assert torch.equal(got, exp), f"replay {i} differs from the eager result"
+
+
+# ------------------------------------------- element-wise tail (bias, residual, ReLU)
+# (kind, n, c, h, w, k, r, s, stride, pad, dil, out_pad); c % 64 == 0 so that the
+# fused path covers them too
+EPI_CASES = [
+    ("conv2d", 2, 64, 9, 11, 72, 3, 3, (1, 1), (1, 1), (1, 1), (0, 0)),
+    ("dilated_conv2d", 1, 128, 12, 10, 48, 3, 3, (1, 1), (2, 2), (2, 2), (0, 0)),
+    ("conv_transpose2d", 2, 64, 5, 6, 40, 4, 4, (2, 2), (1, 1), (1, 1), (0, 0)),
+]
+
+
+def _epi_run(kind, x, wt, stride, pad, dil, out_pad, fuse, **kw):
+    xg, wg = x.to(DEV), wt.to(DEV)
+    if kind == "conv2d":
+        out = ol.derived_conv2d(xg, wg, stride, pad, fuse=fuse, **kw)
+    elif kind == "dilated_conv2d":
+        out = ol.derived_dilated_conv2d(xg, wg, stride, pad, dil, fuse=fuse, **kw)
+    else:
+        out = ol.derived_conv_transpose2d(xg, wg, stride, pad, out_pad, dil, fuse=fuse, **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def _epi_inputs(case, seed, integer, bias_dtype=torch.float32, res_dtype=torch.float32):
+    kind, n, c, h, w, k, r, s, stride, pad, dil, op = case
+    x = synth.random_tensor((n, h, w, c), seed, "bf16", integer=integer)
+    wt = synth.random_tensor((r, s, k, c), seed + 1, "bf16", integer=integer)
+    conv = oracle_conv(kind, x, wt, stride, pad, dil, op)
+    dt = lambda d: "bf16" if d == torch.bfloat16 else "f32"
+    bias = synth.random_tensor((k,), seed + 2, dt(bias_dtype), integer=integer)
+    res = synth.random_tensor(conv.shape, seed + 3, dt(res_dtype), integer=integer)
+    return x, wt, conv, bias, res
+
+
+@pytest.mark.parametrize("ci", range(len(EPI_CASES)))
+@pytest.mark.parametrize("fuse", [False, True])
+@pytest.mark.parametrize("relu", [False, True])
+def test_epilogue_integer_exact(ci, fuse, relu):
+    """Integer-valued inputs, bias and residual: conv + bias + residual is an exact
+    integer, so both paths must equal the definition exactly, ReLU included."""
+    case = EPI_CASES[ci]
+    kind, stride, pad, dil, op = case[0], case[8], case[9], case[10], case[11]
+    say("epilogue", kind, "fuse=%s relu=%s integer" % (fuse, relu))
+    x, wt, conv, bias, res = _epi_inputs(case, 31000 + 10 * ci, True)
+    ref = oracle.conv_epilogue(conv, bias, res, relu)
+    out = _epi_run(kind, x, wt, stride, pad, dil, op, fuse, bias=bias.to(DEV),
+                   residual=res.to(DEV), relu=relu)
+    assert np.array_equal(to_np(out), ref)
+    if relu:
+        assert (ref == 0).any() and (ref > 0).any()
+
+
+@pytest.mark.parametrize("ci", range(len(EPI_CASES)))
+@pytest.mark.parametrize("fuse", [False, True])
+def test_epilogue_terms_and_dtypes(ci, fuse):
+    """Each term alone and in bf16, float inputs, fp32 and bf16 outputs."""
+    case = EPI_CASES[ci]
+    kind, stride, pad, dil, op = case[0], case[8], case[9], case[10], case[11]
+    x, wt, conv, bias, res = _epi_inputs(case, 32000 + 10 * ci, False, torch.bfloat16,
+                                         torch.bfloat16)
+    for kw in ({"bias": bias}, {"residual": res}, {"relu": True},
+               {"bias": bias, "residual": res, "relu": True}):
+        for out_dtype in (torch.float32, torch.bfloat16):
+            say("epilogue", kind, "fuse=%s" % fuse, sorted(kw), out_dtype)
+            ref = oracle.conv_epilogue(conv, kw.get("bias"), kw.get("residual"),
+                                       kw.get("relu", False))
+            gkw = {k2: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k2, v in kw.items()}
+            out = _epi_run(kind, x, wt, stride, pad, dil, op, fuse, out_dtype=out_dtype, **gkw)
+            assert err(to_np(out), ref) <= TOL_BF16
+
+
+@pytest.mark.parametrize("fuse", [False, True])
+def test_epilogue_residual_in_place(fuse):
+    """residual may be the output buffer itself (x + conv written over x)."""
+    case = EPI_CASES[0]
+    kind, stride, pad, dil, op = case[0], case[8], case[9], case[10], case[11]
+    x, wt, conv, bias, res = _epi_inputs(case, 33000, True)
+    ref = oracle.conv_epilogue(conv, bias, res, True)
+    buf = res.to(DEV).clone()
+    out = _epi_run(kind, x, wt, stride, pad, dil, op, fuse, bias=bias.to(DEV), residual=buf,
+                   relu=True, out=buf)
+    assert out.data_ptr() == buf.data_ptr()
+    assert np.array_equal(to_np(buf), ref)
+
+
+def test_epilogue_resnet_workload_fused():
+    """The ResNet conv3x3 workload with the tail of a residual block (bias, identity
+    shortcut, ReLU), fused into the single kernel of the fused expression."""
+    wl = synth.WORKLOADS[2]
+    say("epilogue resnet workload")
+    x, wt = synth.conv_inputs(wl, seed_offset=40)
+    conv = oracle_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil)
+    bias = synth.random_tensor((wl.k,), 34001, "f32")
+    res = synth.random_tensor(conv.shape, 34002, "bf16", dist="normal")
+    ref = oracle.conv_epilogue(conv, bias, res, True)
+    for fuse in (True, False):
+        out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), wl.stride, wl.pad, fuse=fuse,
+                                bias=bias.to(DEV), residual=res.to(DEV), relu=True)
+        torch.cuda.synchronize()
+        assert err(to_np(out), ref) <= TOL_BF16

@@ -376,3 +376,74 @@ def test_band_sampled_rows_match_full():
     assert np.array_equal(s2, s.reshape(-1, 9)[rows])
     assert np.array_equal(p2, p.reshape(-1, 9)[rows])
     assert np.array_equal(o2, o.reshape(-1, 4)[rows])
+
+
+# ------------------------------------------------------ element-wise tail (§6.3)
+
+def _torch_block_tail(conv_t, bias, residual, relu):
+    """The tail as torch builds it: the conv's own bias argument, a tensor add, then
+    torch.relu -- an implementation independent of the oracle's."""
+    y = conv_t
+    if residual is not None:
+        y = y + torch.as_tensor(np.asarray(residual, dtype=np.float64)).permute(0, 3, 1, 2)
+    return torch.relu(y) if relu else y
+
+
+@pytest.mark.parametrize("ci", [0, 1, 4, 6])
+@pytest.mark.parametrize("integer", [False, True])
+@pytest.mark.parametrize("relu", [False, True])
+def test_conv_epilogue_matches_torch_bias_residual_relu(ci, integer, relu):
+    case = CONV_CASES[ci]
+    stride, pad, dil = case[7:10]
+    x, wt = _conv_case_inputs(case, 700 + ci, integer)
+    k = case[4]
+    bias = synth.random_tensor((k,), 720 + ci, integer=integer).numpy()
+    conv = oracle.conv2d(x, wt, stride, pad, dil)
+    residual = synth.random_tensor(conv.shape, 740 + ci, integer=integer).numpy()
+    got = oracle.conv_epilogue(conv, bias, residual, relu)
+    xt = torch.as_tensor(np.asarray(x, dtype=np.float64)).permute(0, 3, 1, 2)
+    wtt = torch.as_tensor(np.asarray(wt, dtype=np.float64)).permute(2, 3, 0, 1)
+    ct = F.conv2d(xt, wtt, bias=torch.as_tensor(bias, dtype=torch.float64), stride=stride,
+                  padding=pad, dilation=dil)
+    ref = _torch_block_tail(ct, bias, residual, relu).permute(0, 2, 3, 1).numpy()
+    if integer:
+        assert np.array_equal(got, ref)
+    else:
+        np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("ci", [0, 2, 4])
+def test_conv_transpose_epilogue_matches_torch(ci):
+    case = CONVT_CASES[ci]
+    stride, pad, dil, op = case[7:11]
+    x, wt = _conv_case_inputs(case, 760 + ci, True)
+    bias = synth.random_tensor((case[4],), 770 + ci, integer=True).numpy()
+    conv = oracle.conv_transpose2d(x, wt, stride, pad, dil, op)
+    residual = synth.random_tensor(conv.shape, 780 + ci, integer=True).numpy()
+    got = oracle.conv_epilogue(conv, bias, residual, True)
+    xt = torch.as_tensor(np.asarray(x, dtype=np.float64)).permute(0, 3, 1, 2)
+    wtt = torch.as_tensor(np.asarray(wt, dtype=np.float64)).permute(3, 2, 0, 1)
+    ct = F.conv_transpose2d(xt, wtt, bias=torch.as_tensor(bias, dtype=torch.float64),
+                            stride=stride, padding=pad, dilation=dil, output_padding=op)
+    ref = _torch_block_tail(ct, bias, residual, True).permute(0, 2, 3, 1).numpy()
+    assert np.array_equal(got, ref)
+
+
+def test_conv_epilogue_terms_one_at_a_time():
+    """Each term on its own: no term is the identity, the bias shifts every pixel of a
+    channel by the same amount, the residual adds elementwise, ReLU zeroes exactly the
+    negative entries and keeps the rest."""
+    rng = np.random.default_rng(5)
+    conv = rng.integers(-9, 10, size=(2, 3, 4, 5)).astype(np.float64)
+    bias = rng.integers(-3, 4, size=(5,)).astype(np.float32)
+    res = rng.integers(-3, 4, size=(2, 3, 4, 5)).astype(np.float32)
+    assert np.array_equal(oracle.conv_epilogue(conv), conv)
+    d = oracle.conv_epilogue(conv, bias=bias) - conv
+    for kk in range(5):
+        assert np.all(d[..., kk] == bias[kk])
+    assert np.array_equal(oracle.conv_epilogue(conv, residual=res) - conv, res)
+    r = oracle.conv_epilogue(conv, relu=True)
+    assert np.all(r >= 0)
+    assert np.array_equal(r[conv > 0], conv[conv > 0])
+    assert np.all(r[conv <= 0] == 0)
+    assert (conv < 0).any() and (conv > 0).any()
