@@ -19,7 +19,8 @@ it runs on.  `roofline` covers the kernel that takes the largest share of a step
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
        python bench.py --stage NAME [--steps K]   (launch one stage kernel K times, for
-       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg>, fused:<cfg> for cfg 2-4, band_fused,
+       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg>, fused:<cfg> for cfg 2-4, fusedres:4
+       (the dilated workload as residue sub-image convolutions), band_fused,
        band_g2bmm, band_softmax, band_gbmm, or copy = a plain 256 MiB device copy)
 """
 from __future__ import annotations
@@ -217,6 +218,11 @@ def main():
                                                  out=op["out"]), reps)
         f_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
                                                **dict(op["kw"], ws=None, fuse=True)), reps)
+        r_ms = None
+        if op["cfg"] == 4:   # the dilated workload also in the residue sub-image form
+            r_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
+                                                   **dict(op["kw"], ws=None, residues=True)),
+                               reps)
         g_tf = op["flops"] / (g_ms * 1e-3) / 1e12
         e_gb = op["eop_bytes"] / (e_ms * 1e-3) / 1e9
         f_tf = op["flops"] / (f_ms * 1e-3) / 1e12
@@ -232,6 +238,8 @@ def main():
             "fused_pct_mfma_peak": round(100 * f_tf / PEAK_BF16_TFLOPS, 2),
             "gemm_gflop": round(op["flops"] / 1e9, 4), "eop_mbytes": round(op["eop_bytes"] / 1e6, 3),
         }
+        if r_ms is not None:
+            per_cfg[name]["fused_residue_form_ms"] = round(r_ms, 5)
         if op["fused"]:
             kernels.append((f"conv_fused[{name}]", f_ms, "mfma", f_tf, PEAK_BF16_TFLOPS,
                             "TFLOP/s", op["flops"]))
@@ -300,6 +308,8 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
             fn = lambda: op["entry"](op["x"], op["wt"], **op["kw"])
         elif kind == "fused":
             fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=True))
+        elif kind == "fusedres":
+            fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], ws=None, residues=True))
     elif name == "band_fused":
         fn = lambda: ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale,
                                    mask_invalid=bwl.mask_invalid, out=o)

@@ -61,6 +61,7 @@ typedef enum {
 #define OLLIE_Y_BF16            (1u << 1)  /* conv: hold the GEMM scope Y in bf16 (default fp32) */
 #define OLLIE_BAND_STAGED       (1u << 2)  /* band: three kernels through S and P in the workspace */
 #define OLLIE_BAND_MASK_INVALID (1u << 3)  /* band: keys outside [0,l) are left out of the softmax */
+#define OLLIE_DILATED_RESIDUES  (1u << 4)  /* dilated conv: as non-dilated convs over residue sub-images */
 
 /* Geometry of a convolution-family operator.
  *   X   [n][h][w][c]   input (NHWC).  As a GEMM operand it is A'[m][c] with
@@ -173,7 +174,14 @@ int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, v
 /* Dilated convolution as the same GEMM plus the dilated OffsetAdd: taps are spaced by
  * the dilation, hi = ho*stride_h - pad_h + r*dil_h, wi = wo*stride_w - pad_w + s*dil_w;
  * taps outside the image read the zero padding and are skipped (boundary tightening,
- * section 4.2).  Same arguments as derived_conv2d; any dil >= 1. */
+ * section 4.2).  Same arguments as derived_conv2d; any dil >= 1.
+ *
+ * OLLIE_DILATED_RESIDUES (with OLLIE_FUSE_EPILOGUE) evaluates instead the derived form
+ * of section 6.2: for stride 1, the outputs of residue (a, b) = (ho % dil_h,
+ * wo % dil_w) are a non-dilated convolution over the input sub-image
+ * X[n][dil_h*i + rho_h][dil_w*j + rho_w], read as a strided view (no copy), so the
+ * operator becomes dil_h*dil_w non-dilated convolutions.  Needs stride 1,
+ * dil_h*dil_w <= 16 and a shape the fused expression covers; else OLLIE_EINVAL. */
 int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt,
                            void* out, void* ws, size_t ws_bytes, uint32_t flags,
                            void* stream);

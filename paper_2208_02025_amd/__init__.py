@@ -26,6 +26,7 @@ FUSE_EPILOGUE = 1 << 0
 Y_BF16 = 1 << 1
 BAND_STAGED = 1 << 2
 BAND_MASK_INVALID = 1 << 3
+DILATED_RESIDUES = 1 << 4
 
 _STATUS_NAMES = {OK: "OLLIE_OK", EINVAL: "OLLIE_EINVAL", EDTYPE: "OLLIE_EDTYPE",
                  EWORKSPACE: "OLLIE_EWORKSPACE", EALIGN: "OLLIE_EALIGN", EHIP: "OLLIE_EHIP"}
@@ -186,14 +187,15 @@ def conv_epilogue(bias=None, residual=None, relu=False):
 
 
 def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output_padding,
-          out_dtype, y_bf16, out, ws, fuse=False, bias=None, residual=None, relu=False):
+          out_dtype, y_bf16, out, ws, fuse=False, bias=None, residual=None, relu=False,
+          extra_flags=0):
     _gpu(x, "x")
     _gpu(wt, "wt")
     if x.dtype != wt.dtype:
         raise ValueError("x and wt must have the same dtype")
     desc = conv_desc(tuple(x.shape), tuple(wt.shape), stride, padding, dilation, output_padding,
                      x.dtype, out_dtype)
-    flags = (Y_BF16 if y_bf16 else 0) | (FUSE_EPILOGUE if fuse else 0)
+    flags = (Y_BF16 if y_bf16 else 0) | (FUSE_EPILOGUE if fuse else 0) | extra_flags
     ho, wo = conv_out_hw(desc, transposed)
     if out is None:
         out = torch.empty((desc.n, ho, wo, desc.k), dtype=out_dtype, device=x.device)
@@ -233,10 +235,13 @@ def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=F
 
 def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,
                            y_bf16=False, out=None, ws=None, fuse=False, bias=None,
-                           residual=None, relu=False):
-    """Dilated Conv2d as GEMM + dilated OffsetAdd eOperator."""
+                           residual=None, relu=False, residues=False):
+    """Dilated Conv2d as GEMM + dilated OffsetAdd eOperator.  residues=True (implies
+    fuse=True) evaluates it as dil_h*dil_w non-dilated convolutions over the residue
+    sub-images of the input instead (stride 1)."""
     return _conv("derived_dilated_conv2d", False, x, wt, stride, padding, dilation, 0,
-                 out_dtype, y_bf16, out, ws, fuse, bias, residual, relu)
+                 out_dtype, y_bf16, out, ws, fuse or residues, bias, residual, relu,
+                 DILATED_RESIDUES if residues else 0)
 
 
 def derived_conv_transpose2d(x, wt, stride=1, padding=0, output_padding=0, dilation=1,

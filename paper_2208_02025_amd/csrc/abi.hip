@@ -92,10 +92,14 @@ ConvGeom conv_geom(const ollie_conv_desc* d, int64_t ho, int64_t wo) {
     return g;
 }
 
+int conv_form(int transposed, uint32_t flags) {
+    return transposed ? kTransposed : (flags & OLLIE_DILATED_RESIDUES) ? kResidues : kForward;
+}
+
 bool fused_path(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
                 uint32_t flags) {
     return (flags & OLLIE_FUSE_EPILOGUE) && d->in_dtype == OLLIE_BF16 &&
-           conv_fused_supported(conv_geom(d, ho, wo), transposed);
+           conv_fused_supported(conv_geom(d, ho, wo), conv_form(transposed, flags));
 }
 
 size_t conv_ws(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
@@ -144,16 +148,21 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     Epi epi;
     st = make_epi(epilogue, &epi);
     if (st) return st;
-    if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE))
+    if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE | OLLIE_DILATED_RESIDUES))
         return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
     if (!x || !wt || !out) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!dtype_ok(d->in_dtype) || !dtype_ok(d->out_dtype))
         return fail(OLLIE_EDTYPE, "in_dtype/out_dtype must be OLLIE_F32 or OLLIE_BF16");
+    if ((flags & OLLIE_DILATED_RESIDUES) && !fused_path(d, transposed, ho, wo, flags))
+        return fail(OLLIE_EINVAL,
+                    "OLLIE_DILATED_RESIDUES needs OLLIE_FUSE_EPILOGUE, stride 1, bf16 inputs, "
+                    "c %% 64 == 0 and dil_h*dil_w <= 16");
     if (fused_path(d, transposed, ho, wo, flags)) {
         if (!aligned16(x) || !aligned16(wt) || !aligned16(out))
             return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
-        hipError_t e = launch_conv_fused(conv_geom(d, ho, wo), transposed, x, wt, out,
-                                         d->out_dtype == OLLIE_BF16, epi, (hipStream_t)stream);
+        hipError_t e = launch_conv_fused(conv_geom(d, ho, wo), conv_form(transposed, flags), x,
+                                         wt, out, d->out_dtype == OLLIE_BF16, epi,
+                                         (hipStream_t)stream);
         if (e != hipSuccess) return hip_fail(e, "fused GEMM+eOperator launch");
         return OLLIE_OK;
     }
@@ -245,6 +254,8 @@ int derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt
                       void* ws, size_t ws_bytes, uint32_t flags,
                       const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
+    if (flags & OLLIE_DILATED_RESIDUES)
+        return fail(OLLIE_EINVAL, "OLLIE_DILATED_RESIDUES applies to derived_dilated_conv2d");
     if (desc && (desc->dil_h != 1 || desc->dil_w != 1))
         return fail(OLLIE_EINVAL, "derived_conv2d takes dilation 1; use derived_dilated_conv2d");
     return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
@@ -261,6 +272,8 @@ int derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, cons
                                 void* out, void* ws, size_t ws_bytes, uint32_t flags,
                                 const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
+    if (flags & OLLIE_DILATED_RESIDUES)
+        return fail(OLLIE_EINVAL, "OLLIE_DILATED_RESIDUES applies to derived_dilated_conv2d");
     return conv_common(desc, 1, x, wt, out, ws, ws_bytes, flags, epi, stream);
 }
 

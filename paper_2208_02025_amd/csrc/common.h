@@ -138,10 +138,14 @@ struct ConvGeom {
 hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, int y_bf16,
                              void* out, int out_bf16, const Epi& epi, hipStream_t stream);
 
-// Fused GEMM + eOperator (output-stationary), bf16 operands.  Returns
-// hipErrorInvalidValue when the shape is outside what the fused kernel supports.
-bool conv_fused_supported(const ConvGeom& g, int transposed);
-hipError_t launch_conv_fused(const ConvGeom& g, int transposed, const void* x, const void* wt,
+// Fused GEMM + eOperator (output-stationary), bf16 operands.  form: the derived
+// program evaluated -- the forward convolution, the transposed convolution, or a
+// stride-1 dilated convolution as dil_h*dil_w non-dilated convolutions over the
+// residue sub-images of the input.  Returns hipErrorInvalidValue when the shape is
+// outside what the fused kernel supports.
+enum ConvForm { kForward = 0, kTransposed = 1, kResidues = 2 };
+bool conv_fused_supported(const ConvGeom& g, int form);
+hipError_t launch_conv_fused(const ConvGeom& g, int form, const void* x, const void* wt,
                              void* out, int out_bf16, const Epi& epi, hipStream_t stream);
 
 struct BandGeom {

@@ -17,8 +17,11 @@
 //                     belongs to the class iff (ho + pad - r*dil) is divisible by the
 //                     stride, and then hi = ho/stride + (ho%stride + pad - r*dil)/stride.
 //                     Each class contracts over its own taps only, so no partial that the
-//                     selective add would drop is ever computed.
-// Both cases are  hi = alpha*i + beta_tap,  ho = oh0 + gamma*i  over class coordinates i.
+//                     selective add would drop is ever computed;
+//   dilated conv as residue sub-images (stride 1, section 6.2): one class per output
+//                     residue (ho % dil, wo % dil), a non-dilated convolution over the
+//                     input sub-image of the matching residue (alpha = gamma = dil).
+// All cases are  hi = alpha*i + beta_tap,  ho = oh0 + gamma*i  over class coordinates i.
 //
 // Main loop: the bf16 DMA pipeline of the GEMM stage (global_load_lds_dwordx4 into an
 // XOR-swizzled LDS ring, v_mfma_f32_16x16x32_bf16).  A rows are gathered per tap; rows
@@ -32,7 +35,7 @@ namespace ollie {
 namespace {
 
 constexpr int kMaxCls = 16;
-constexpr int kMaxTaps = 64;
+constexpr int kMaxTaps = 144;
 
 __device__ __align__(16) uint32_t kZeroChunk[4];   // 16 zero bytes (zero-initialised)
 
@@ -194,12 +197,38 @@ void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ 
 }
 
 // Host-side plan: classes, their tap lists, and the tile count for a BM x BN tiling.
-bool make_plan(const ConvGeom& g, int transposed, FusedPlan& P) {
+bool make_plan(const ConvGeom& g, int form, FusedPlan& P) {
     P = FusedPlan{};
     P.n = (int)g.n; P.c = (int)g.c; P.h = (int)g.h; P.w = (int)g.w; P.k = (int)g.k;
     P.ho = (int)g.ho; P.wo = (int)g.wo;
     int ntaps = 0, ncls = 0;
-    if (!transposed) {
+    if (form == kResidues) {
+        // Dilated convolution with stride 1 as dil_h*dil_w non-dilated convolutions
+        // (section 6.2): output (a + dh*i, b + dw*j) reads input row
+        // dh*i + (a - ph + r*dh), i.e. row i + r of the residue sub-image with offset
+        // a - ph, read through a strided view (no copy).  One class per (a, b).
+        if (g.sh != 1 || g.sw != 1 || (int64_t)g.dh * g.dw > kMaxCls) return false;
+        P.alpha_h = g.dh; P.alpha_w = g.dw; P.gam_h = g.dh; P.gam_w = g.dw;
+        for (int ah = 0; ah < g.dh; ++ah)
+            for (int aw = 0; aw < g.dw; ++aw) {
+                const int hc = ah < g.ho ? (int)((g.ho - ah + g.dh - 1) / g.dh) : 0;
+                const int wc = aw < g.wo ? (int)((g.wo - aw + g.dw - 1) / g.dw) : 0;
+                if (hc == 0 || wc == 0) continue;
+                P.cls_hc[ncls] = hc; P.cls_wc[ncls] = wc;
+                P.cls_oh0[ncls] = ah; P.cls_ow0[ncls] = aw;
+                P.cls_tap0[ncls] = ntaps;
+                for (int r = 0; r < g.r; ++r)
+                    for (int s = 0; s < g.s; ++s) {
+                        if (ntaps >= kMaxTaps) return false;
+                        P.tap_bh[ntaps] = ah - g.ph + r * g.dh;
+                        P.tap_bw[ntaps] = aw - g.pw + s * g.dw;
+                        P.tap_rs[ntaps] = (int)(r * g.s + s);
+                        ++ntaps;
+                    }
+                ++ncls;
+            }
+        P.cls_tap0[ncls] = ntaps;
+    } else if (form == kForward) {
         P.alpha_h = g.sh; P.alpha_w = g.sw; P.gam_h = 1; P.gam_w = 1;
         P.cls_hc[0] = (int)g.ho; P.cls_wc[0] = (int)g.wo; P.cls_oh0[0] = 0; P.cls_ow0[0] = 0;
         P.cls_tap0[0] = 0;
@@ -292,16 +321,16 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
 
 }  // namespace
 
-bool conv_fused_supported(const ConvGeom& g, int transposed) {
+bool conv_fused_supported(const ConvGeom& g, int form) {
     if (g.c % kTileK != 0) return false;
     FusedPlan P;
-    return make_plan(g, transposed, P);
+    return make_plan(g, form, P);
 }
 
-hipError_t launch_conv_fused(const ConvGeom& g, int transposed, const void* x, const void* wt,
+hipError_t launch_conv_fused(const ConvGeom& g, int form, const void* x, const void* wt,
                              void* out, int out_bf16, const Epi& epi, hipStream_t stream) {
     FusedPlan P;
-    if (g.c % kTileK != 0 || !make_plan(g, transposed, P)) return hipErrorInvalidValue;
+    if (g.c % kTileK != 0 || !make_plan(g, form, P)) return hipErrorInvalidValue;
     return out_bf16 ? dispatch<bf16_t>(P, x, wt, out, epi, stream)
                     : dispatch<float>(P, x, wt, out, epi, stream);
 }

@@ -240,3 +240,18 @@ def test_library_exports_nothing_else(lib):
                          text=True, check=True)
     funcs = {ln.split()[-1] for ln in res.stdout.splitlines() if " T " in ln}
     assert funcs == set(header_functions())
+
+
+def test_residue_flag_rejections(lib):
+    def call(entry, d, flags):
+        return getattr(lib, entry)(ctypes.byref(d), A16, B16, C16, W16, 1 << 40, flags, None)
+    R = ol.DILATED_RESIDUES | ol.FUSE_EPILOGUE
+    d_ok = conv(c=64, dil=2, pad=2)
+    assert call("derived_conv2d", conv(c=64), R) == ol.EINVAL                 # wrong entry
+    assert call("derived_conv_transpose2d", conv(c=64, stride=2), R) == ol.EINVAL
+    assert call("derived_dilated_conv2d", d_ok, ol.DILATED_RESIDUES) == ol.EINVAL  # no fuse
+    assert call("derived_dilated_conv2d", conv(c=64, dil=2, pad=2, stride=2), R) == ol.EINVAL
+    assert call("derived_dilated_conv2d", conv(c=32, dil=2, pad=2), R) == ol.EINVAL
+    assert call("derived_dilated_conv2d", conv(c=64, dil=5, pad=5), R) == ol.EINVAL
+    assert call("derived_dilated_conv2d", conv(c=64, dil=2, pad=2, in_dtype=ol.F32), R) == ol.EINVAL
+    assert ol.conv_workspace_bytes(d_ok, False, R) == 0

@@ -616,3 +616,58 @@ def test_epilogue_resnet_workload_fused():
                                 bias=bias.to(DEV), residual=res.to(DEV), relu=True)
         torch.cuda.synchronize()
         assert err(to_np(out), ref) <= TOL_BF16
+
+
+# ------------------------------- dilated conv as residue sub-image convolutions (§6.2)
+# (n, c, h, w, k, dil, pad); stride 1, 3x3
+RESIDUE_CASES = [
+    (1, 64, 14, 18, 40, (2, 2), (2, 2)),
+    (2, 128, 11, 9, 72, (3, 2), (1, 2)),     # ragged classes, asymmetric dilation
+    (1, 64, 13, 13, 64, (4, 4), (4, 4)),     # 16 classes x 9 taps
+    (1, 64, 7, 10, 24, (2, 3), (0, 0)),      # no padding
+]
+
+
+@pytest.mark.parametrize("ci", range(len(RESIDUE_CASES)))
+def test_residue_form_integer_exact(ci):
+    n, c, h, w, k, dil, pad = RESIDUE_CASES[ci]
+    say("residue form", RESIDUE_CASES[ci])
+    x = synth.random_tensor((n, h, w, c), 35000 + ci, "bf16", integer=True)
+    wt = synth.random_tensor((3, 3, k, c), 35100 + ci, "bf16", integer=True)
+    ref = oracle.conv2d(x, wt, (1, 1), pad, dil)
+    out = ol.derived_dilated_conv2d(x.to(DEV), wt.to(DEV), 1, pad, dil, residues=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out), ref)
+
+
+def test_residue_form_workload_and_tail():
+    """The CSRNet workload in the residue form: against the oracle, against the
+    default fused form, and with a bias + ReLU tail."""
+    wl = synth.WORKLOADS[4]
+    say("residue form workload")
+    x, wt = synth.conv_inputs(wl, seed_offset=50)
+    ref = oracle_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil)
+    xg, wg = x.to(DEV), wt.to(DEV)
+    out = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, residues=True)
+    base = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, fuse=True)
+    torch.cuda.synchronize()
+    assert err(to_np(out), ref) <= TOL_BF16
+    # same taps summed in the same order: the two schedules agree bit for bit
+    assert torch.equal(out, base)
+    bias = synth.random_tensor((wl.k,), 35201, "f32")
+    out = ol.derived_dilated_conv2d(xg, wg, wl.stride, wl.pad, wl.dil, residues=True,
+                                    bias=bias.to(DEV), relu=True)
+    torch.cuda.synchronize()
+    assert err(to_np(out), oracle.conv_epilogue(ref, bias, None, True)) <= TOL_BF16
+
+
+def test_residue_form_rejections():
+    x = torch.zeros((1, 9, 9, 64), dtype=torch.bfloat16, device=DEV)
+    wt = torch.zeros((3, 3, 8, 64), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(ol.OllieError):
+        ol.derived_dilated_conv2d(x, wt, 2, 2, 2, residues=True)          # stride 2
+    with pytest.raises(ol.OllieError):
+        ol.derived_dilated_conv2d(x, wt, 1, 5, 5, residues=True)          # 25 classes
+    with pytest.raises(ol.OllieError):
+        ol.derived_dilated_conv2d(x[..., :32].contiguous(), wt[..., :32].contiguous(), 1, 2, 2,
+                                  residues=True)                          # c % 64 != 0

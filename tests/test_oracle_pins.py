@@ -447,3 +447,34 @@ def test_conv_epilogue_terms_one_at_a_time():
     assert np.array_equal(r[conv > 0], conv[conv > 0])
     assert np.all(r[conv <= 0] == 0)
     assert (conv < 0).any() and (conv > 0).any()
+
+
+# ------------------------------- dilated conv = non-dilated convs of sub-images (§6.2)
+
+@pytest.mark.parametrize("dil,pad,hw", [((2, 2), (2, 2), (9, 12)), ((3, 2), (1, 2), (10, 7)),
+                                        ((2, 3), (0, 3), (8, 11)), ((4, 4), (4, 4), (13, 13))])
+def test_dilated_conv_is_residue_subimage_convs(dil, pad, hw):
+    """With stride 1, the outputs of residue (a, b) = (ho % dh, wo % dw) are the
+    non-dilated convolution of the input sub-image of residue ((a - ph) mod dh,
+    (b - pw) mod dw), shifted by floor((a - ph) / dh) rows (likewise for columns)."""
+    n, c, k, r, s = 2, 3, 2, 3, 3
+    h, w = hw
+    x = synth.random_tensor((n, h, w, c), 801, integer=True).numpy()
+    wt = synth.random_tensor((r, s, k, c), 802, integer=True).numpy()
+    full = oracle.conv2d(x, wt, (1, 1), pad, dil)
+    ho, wo = full.shape[1:3]
+    dh, dw = dil
+    for a in range(min(dh, ho)):
+        for b in range(min(dw, wo)):
+            qh, rh = divmod(a - pad[0], dh)
+            qw, rw = divmod(b - pad[1], dw)
+            sub = x[:, rh::dh, rw::dw, :]
+            hc, wc = len(range(a, ho, dh)), len(range(b, wo, dw))
+            # zero-extend the sub-image so that rows qh .. qh + hc + r - 2 exist
+            lo_h, lo_w = max(0, -qh), max(0, -qw)
+            hi_h = max(0, qh + hc + r - 1 - sub.shape[1])
+            hi_w = max(0, qw + wc + s - 1 - sub.shape[2])
+            padded = np.pad(sub, ((0, 0), (lo_h, hi_h), (lo_w, hi_w), (0, 0)))
+            win = padded[:, qh + lo_h: qh + lo_h + hc + r - 1, qw + lo_w: qw + lo_w + wc + s - 1]
+            part = oracle.conv2d(win, wt, (1, 1), (0, 0), (1, 1))
+            assert np.array_equal(part, full[:, a::dh, b::dw, :])
