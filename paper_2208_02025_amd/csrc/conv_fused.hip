@@ -296,8 +296,10 @@ hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, const Epi&
     return hipGetLastError();
 }
 
-// 0 = 128x128 with 8 waves (two workgroups per CU), 1 = 64x128 with 4 waves, 2 = 64x64
-// with 8 waves; OLLIE_FUSED_CONFIG overrides the shape-based choice for tuning sweeps.
+// Tile shapes, largest first: 0 = 192x128 with 8 waves (one workgroup per CU),
+// 1 = 128x128 with 8 waves (two per CU), 2 = 64x128 with 4 waves, 3 = 64x64 with 8 waves.
+// The first with at least ~one tile per CU is taken; OLLIE_FUSED_CONFIG overrides the
+// choice for tuning sweeps.
 template <typename OT>
 hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
                     hipStream_t st) {
@@ -306,15 +308,17 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
         return e ? atoi(e) : -1;
     }();
     int cfg = forced;
-    if (cfg < 0 || cfg > 2) {
+    if (cfg < 0 || cfg > 3) {
         FusedPlan tmp = P;
-        if (plan_tiles(tmp, 128, 128) >= 240) cfg = 0;
-        else if (plan_tiles(tmp, 64, 128) >= 240) cfg = 1;
-        else cfg = 2;
+        if (plan_tiles(tmp, 192, 128) >= 240) cfg = 0;
+        else if (plan_tiles(tmp, 128, 128) >= 240) cfg = 1;
+        else if (plan_tiles(tmp, 64, 128) >= 240) cfg = 2;
+        else cfg = 3;
     }
     switch (cfg) {
-    case 0: return go<128, 128, 2, OT, 8>(P, x, wt, out, epi, st);
-    case 1: return go<64, 128, 2, OT, 4>(P, x, wt, out, epi, st);
+    case 0: return go<192, 128, 2, OT, 8>(P, x, wt, out, epi, st);
+    case 1: return go<128, 128, 2, OT, 8>(P, x, wt, out, epi, st);
+    case 2: return go<64, 128, 2, OT, 4>(P, x, wt, out, epi, st);
     default: return go<64, 64, 2, OT, 8>(P, x, wt, out, epi, st);
     }
 }
