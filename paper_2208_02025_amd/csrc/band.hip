@@ -305,10 +305,10 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
 // and probabilities stay in registers.  A wave owns 32 queries (two 16-query halves hq),
 // a workgroup 128.  Key/value blocks of 64 rows reach LDS by direct global->LDS copies
 // (global_load_lds_dwordx4) into a ring of kSlots blocks, issued kSlots - 1 blocks
-// ahead.  Each block iteration computes the softmax and P*V of block kb while the
-// scores of block kb + 1 are computed by MFMA between its exp2 instructions, so the
-// matrix unit and the vector ALU work side by side; the loop is unrolled by two so the
-// two score buffers alternate without register copies.
+// ahead.  The kernel is latency-bound, so it is sized for occupancy rather than
+// intra-wave overlap: with two slots (32 KB of LDS per workgroup) and <= 128 VGPRs,
+// four workgroups share a CU and four waves each SIMD, whose independent block
+// iterations hide each other's LDS, MFMA and exp2 latencies.
 //
 // Softmax bookkeeping per query, in log2 units (x = scale*log2(e)*score): a running
 // reference m, and the denominator and O both accumulated unnormalised by MFMA -- the
@@ -353,7 +353,7 @@ __device__ __forceinline__ void block_sync() {
 }
 
 template <typename OT, bool MASK, int kSlots>
-__global__ __launch_bounds__(256, 2) void band_fused_kernel(BandGeom g, int ntx,
+__global__ __launch_bounds__(256, 4) void band_fused_kernel(BandGeom g, int ntx,
                                                            const bf16_t* __restrict__ Q,
                                                            const bf16_t* __restrict__ K,
                                                            const bf16_t* __restrict__ V,
@@ -463,7 +463,7 @@ __global__ __launch_bounds__(256, 2) void band_fused_kernel(BandGeom g, int ntx,
     const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)lds;
     // waits until at most `later` blocks (4 copies each per lane) are still in flight
     auto wait_blocks = [](int later) {
-        static_assert(kSlots >= 3 && kSlots <= 6, "slot count");
+        static_assert(kSlots >= 2 && kSlots <= 6, "slot count");
         if (later >= 3 && kSlots >= 6) wait_vmcnt<12>();
         else if (later >= 2 && kSlots >= 5) wait_vmcnt<8>();
         else if (later >= 1) wait_vmcnt<4>();
@@ -502,12 +502,15 @@ __global__ __launch_bounds__(256, 2) void band_fused_kernel(BandGeom g, int ntx,
             }
     };
 
-    // One block iteration: softmax and P*V of block kb (scores in s) while the scores
-    // of block kb + 1 are computed into sn (at the wave's last block they are not used).
-    auto step = [&](int kb, f32x4 (&s)[2][4], f32x4 (&sn)[2][4]) {
+    // One block iteration: scores, softmax and P*V of block kb.
+    auto step = [&](int kb) {
         const int t0 = t.q0 - w + kb * kT;
-        bf16x8 kf[4][2];
-        read_k(kb + 1, kf);
+        f32x4 s[2][4];
+        {
+            bf16x8 kf[4][2];
+            read_k(kb, kf);
+            scores(kf, s);
+        }
         bool full = t0 >= qa + kQW - 1 - w && t0 + kT - 1 <= qa + w;
         if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
         if (!full) {                               // band (and range) mask, in place
@@ -553,7 +556,6 @@ __global__ __launch_bounds__(256, 2) void band_fused_kernel(BandGeom g, int ntx,
                 m_run[hq] = m_new;
             }
         }
-        scores(kf, sn);
         bf16x8 pf[2][2];
 #pragma unroll
         for (int hq = 0; hq < 2; ++hq) {
@@ -594,36 +596,19 @@ __global__ __launch_bounds__(256, 2) void band_fused_kernel(BandGeom g, int ntx,
                                                                    0, 0, 0);
         }
     };
-    // One loop iteration over block kb: prefetch, compute (if the block meets the
-    // wave's band), then make block kb + 2 resident for the next iteration.
-    auto iter = [&](int kb, f32x4 (&s)[2][4], f32x4 (&sn)[2][4]) {
-        if (kb + kSlots - 1 < nblk) dma(kb + kSlots - 1);
-        if (kb >= lo && kb <= hi) {
-            if (kb == lo) {                        // the wave's first block
-                bf16x8 kf[4][2];
-                read_k(kb, kf);
-                scores(kf, s);
-            }
-            step(kb, s, sn);
-        }
-        // block kb + 2 is read by the next iteration: its copies must have landed; those
-        // of the blocks after it may still be in flight
-        wait_blocks(min(nblk - 1, kb + kSlots - 1) - (kb + 2));
-        block_sync();
-    };
-
-    // prologue: blocks 0 .. kSlots-2 in flight; blocks 0 and 1 resident before the loop
+    // prologue: blocks 0 .. kSlots-2 in flight, block 0 resident before the loop
 #pragma unroll
     for (int b = 0; b < kSlots - 1; ++b)
         if (b < nblk) dma(b);
-    wait_blocks(min(nblk - 1, kSlots - 2) - 1);
+    wait_blocks(min(nblk - 1, kSlots - 2));
     block_sync();
-    // unrolled by two so the two score buffers alternate without register copies
-    f32x4 sa[2][4], sb[2][4];
-    for (int kb = 0; kb < nblk; kb += 2) {
-        iter(kb, sa, sb);
-        if (kb + 1 >= nblk) break;
-        iter(kb + 1, sb, sa);
+    for (int kb = 0; kb < nblk; ++kb) {
+        if (kb + kSlots - 1 < nblk) dma(kb + kSlots - 1);
+        if (kb >= lo && kb <= hi) step(kb);          // the block meets the wave's band
+        // block kb + 1 is read by the next iteration: its copies must have landed; those
+        // of the blocks after it may still be in flight
+        wait_blocks(min(nblk - 1, kb + kSlots - 1) - (kb + 1));
+        block_sync();
     }
 #pragma unroll
     for (int hq = 0; hq < 2; ++hq) {
@@ -693,7 +678,7 @@ hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, co
     const int ntx = (int)((l0 + 127) / 128);
     const dim3 grid((unsigned)(ntx * g.dil * g.b));
 #define OLLIE_FUSED(OT, M)                                                                   \
-    hipLaunchKernelGGL((band_fused_kernel<OT, M, 4>), grid, dim3(256), 0, stream, g, ntx,     \
+    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2>), grid, dim3(256), 0, stream, g, ntx,     \
                        (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
     if (o_bf16) {
         if (mask) OLLIE_FUSED(bf16_t, true);
