@@ -352,8 +352,8 @@ __device__ __forceinline__ void block_sync() {
     asm volatile("" ::: "memory");
 }
 
-template <typename OT, bool MASK, int kSlots>
-__global__ __launch_bounds__(256, 4) void band_fused_kernel(BandGeom g, int ntx,
+template <typename OT, bool MASK, int kSlots, int NW>
+__global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int ntx,
                                                            const bf16_t* __restrict__ Q,
                                                            const bf16_t* __restrict__ K,
                                                            const bf16_t* __restrict__ V,
@@ -364,7 +364,8 @@ __global__ __launch_bounds__(256, 4) void band_fused_kernel(BandGeom g, int ntx,
     // margin means the reference settles after the first block and rescaling is rare.
     constexpr float kLazy = 64.f;
     constexpr int kQW = 32;               // queries per wave
-    constexpr int kFT = 4 * kQW;          // queries per tile
+    constexpr int kFT = NW * kQW;         // queries per tile (NW waves)
+    constexpr int kPass = 64 / (NW * 8);  // copy instructions per lane per 64-row block
     __shared__ u32x4 lds[kSlots * kSlotChunks];
     Tile t;
     {
@@ -406,7 +407,7 @@ __global__ __launch_bounds__(256, 4) void band_fused_kernel(BandGeom g, int ntx,
     const int lo = wv * kQW / kT;
     const int hi = min(nblk - 1, (wv * kQW + kQW - 1 + 2 * w) / kT);
 
-    // DMA sources of this lane: key rows dr and dr + 32 of each block, chunk dch, as byte
+    // DMA sources of this lane: key rows dr + e*NW*8 of each block, chunk dch, as byte
     // offsets from the start of the residue subsequence (uniform base pointers)
     const int dr = wv * 8 + (lane >> 3);
     const int dch = (lane & 7) ^ ((lane >> 3) & 7);
@@ -423,24 +424,26 @@ __global__ __launch_bounds__(256, 4) void band_fused_kernel(BandGeom g, int ntx,
         const uint32_t off = boff + (uint32_t)(kb * kT) * row_bytes;
         if (t.q0 - w + kb * kT >= 0 && t.q0 - w + kb * kT + kT <= t.lr) {   // interior block
 #pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const uint32_t o2 = off + e * 32 * row_bytes;
+            for (int e = 0; e < kPass; ++e) {
+                const uint32_t o2 = off + e * NW * 8 * row_bytes;
                 __builtin_amdgcn_global_load_lds((const void*)(kseq + o2),
-                                                 (lds_void*)(slot + e * 256 + wv * 64), 16, 0, 0);
+                                                 (lds_void*)(slot + (e * NW + wv) * 64), 16, 0,
+                                                 0);
                 __builtin_amdgcn_global_load_lds((const void*)(vseq + o2),
-                                                 (lds_void*)(slot + 512 + e * 256 + wv * 64),
+                                                 (lds_void*)(slot + 512 + (e * NW + wv) * 64),
                                                  16, 0, 0);
             }
         } else {
 #pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const int te = tt + 32 * e;
+            for (int e = 0; e < kPass; ++e) {
+                const int te = tt + NW * 8 * e;
                 const bool ok = te >= 0 && te < t.lr;
                 const uint32_t o2 = (uint32_t)te * row_bytes + dch * 16;
                 __builtin_amdgcn_global_load_lds((const void*)(ok ? kseq + o2 : zero),
-                                                 (lds_void*)(slot + e * 256 + wv * 64), 16, 0, 0);
+                                                 (lds_void*)(slot + (e * NW + wv) * 64), 16, 0,
+                                                 0);
                 __builtin_amdgcn_global_load_lds((const void*)(ok ? vseq + o2 : zero),
-                                                 (lds_void*)(slot + 512 + e * 256 + wv * 64),
+                                                 (lds_void*)(slot + 512 + (e * NW + wv) * 64),
                                                  16, 0, 0);
             }
         }
@@ -461,12 +464,13 @@ __global__ __launch_bounds__(256, 4) void band_fused_kernel(BandGeom g, int ntx,
     }
     const char* lds_b = reinterpret_cast<const char*>(lds);
     const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)lds;
-    // waits until at most `later` blocks (4 copies each per lane) are still in flight
+    // waits until at most `later` blocks (2*kPass copies each per lane) are in flight
     auto wait_blocks = [](int later) {
         static_assert(kSlots >= 2 && kSlots <= 6, "slot count");
-        if (later >= 3 && kSlots >= 6) wait_vmcnt<12>();
-        else if (later >= 2 && kSlots >= 5) wait_vmcnt<8>();
-        else if (later >= 1) wait_vmcnt<4>();
+        constexpr int kC = 2 * kPass;
+        if (later >= 3 && kSlots >= 6) wait_vmcnt<3 * kC>();
+        else if (later >= 2 && kSlots >= 5) wait_vmcnt<2 * kC>();
+        else if (later >= 1) wait_vmcnt<kC>();
         else wait_vmcnt<0>();
     };
 
@@ -672,14 +676,15 @@ hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, voi
     return hipGetLastError();
 }
 
-hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
-                             void* o, int o_bf16, int mask, hipStream_t stream) {
+template <int NW>
+hipError_t launch_fused_nw(const BandGeom& g, const void* q, const void* k, const void* v,
+                           void* o, int o_bf16, int mask, hipStream_t stream) {
     const int64_t l0 = (g.l + g.dil - 1) / g.dil;
-    const int ntx = (int)((l0 + 127) / 128);
+    const int ntx = (int)((l0 + 32 * NW - 1) / (32 * NW));
     const dim3 grid((unsigned)(ntx * g.dil * g.b));
 #define OLLIE_FUSED(OT, M)                                                                   \
-    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2>), grid, dim3(256), 0, stream, g, ntx,     \
-                       (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
+    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2, NW>), grid, dim3(64 * NW), 0, stream, g,  \
+                       ntx, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
     if (o_bf16) {
         if (mask) OLLIE_FUSED(bf16_t, true);
         else OLLIE_FUSED(bf16_t, false);
@@ -689,6 +694,13 @@ hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, co
     }
 #undef OLLIE_FUSED
     return hipGetLastError();
+}
+
+// Four waves per workgroup: measured faster than eight (half the copies per query, but
+// the same occupancy and twice the LDS per workgroup).
+hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
+                             void* o, int o_bf16, int mask, hipStream_t stream) {
+    return launch_fused_nw<4>(g, q, k, v, o, o_bf16, mask, stream);
 }
 
 }  // namespace ollie
