@@ -297,7 +297,8 @@ hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, const Epi&
 }
 
 // Tile shapes, largest first: 0 = 192x128 with 8 waves (one workgroup per CU),
-// 1 = 128x128 with 8 waves (two per CU), 2 = 64x128 with 4 waves, 3 = 64x64 with 8 waves.
+// 1 = 128x128 with 8 waves (two per CU), 2 = 64x128 with 4 waves, 3 = 64x64 with 8 waves
+// and a 4-stage copy ring.
 // The first with at least ~one tile per CU is taken; OLLIE_FUSED_CONFIG overrides the
 // choice for tuning sweeps.
 template <typename OT>
@@ -319,7 +320,9 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
     case 0: return go<192, 128, 2, OT, 8>(P, x, wt, out, epi, st);
     case 1: return go<128, 128, 2, OT, 8>(P, x, wt, out, epi, st);
     case 2: return go<64, 128, 2, OT, 4>(P, x, wt, out, epi, st);
-    default: return go<64, 64, 2, OT, 8>(P, x, wt, out, epi, st);
+    // the small shapes run right after other kernels have evicted their operands: a
+    // 4-deep copy ring hides the longer cold loads (measured in the benchmark step)
+    default: return go<64, 64, 4, OT, 8>(P, x, wt, out, epi, st);
     }
 }
 
