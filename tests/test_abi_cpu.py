@@ -255,3 +255,27 @@ def test_residue_flag_rejections(lib):
     assert call("derived_dilated_conv2d", conv(c=64, dil=5, pad=5), R) == ol.EINVAL
     assert call("derived_dilated_conv2d", conv(c=64, dil=2, pad=2, in_dtype=ol.F32), R) == ol.EINVAL
     assert ol.conv_workspace_bytes(d_ok, False, R) == 0
+
+
+def test_validation_never_lets_a_bad_descriptor_through(lib):
+    """Randomised descriptors with invalid fields: every call returns a non-zero status
+    with a message before any HIP call (fake device pointers are never touched)."""
+    import random
+    rng = random.Random(7)
+    bad = 0
+    for _ in range(400):
+        d = conv(n=rng.choice([0, 1, 2, -1]), c=rng.choice([0, 16, 64, -5]),
+                 h=rng.choice([0, 1, 7]), w=rng.choice([1, 9, 0]), k=rng.choice([0, 8, -1]),
+                 r=rng.choice([0, 1, 3, 9]), s=rng.choice([1, 3, -2]),
+                 stride=rng.choice([0, 1, 2]), pad=rng.choice([-1, 0, 1, 4]),
+                 dil=rng.choice([0, 1, 2]), op=rng.choice([0, 1, 3]),
+                 in_dtype=rng.choice([ol.BF16, ol.F32, 5]), out_dtype=rng.choice([ol.F32, 9]))
+        invalid = (min(d.n, d.c, d.h, d.w, d.k, d.r, d.s) < 1 or d.stride_h < 1 or d.dil_h < 1
+                   or d.pad_h < 0 or d.in_dtype not in (0, 1) or d.out_dtype not in (0, 1))
+        if not invalid:
+            continue
+        bad += 1
+        for entry in ("derived_conv2d", "derived_dilated_conv2d", "derived_conv_transpose2d"):
+            st, msg = call_conv(lib, entry, d)
+            assert st != ol.OK and msg, (entry, st)
+    assert bad > 100
