@@ -33,9 +33,17 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found; the ROCm toolchain is required to build libollie.so")
 
 
+# Per-source extra flags.  The large fused-convolution tiles keep 96 accumulator
+# registers per lane live next to two operand-fragment sets; the VGPR form of the MFMA
+# keeps them in place (with accumulators in AGPRs the register allocator shuffled them
+# between the two register files every iteration).
+SOURCE_FLAGS = {"conv_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *HIPCC_FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
