@@ -352,7 +352,7 @@ __device__ __forceinline__ void block_sync() {
     asm volatile("" ::: "memory");
 }
 
-template <typename OT, bool MASK, int kSlots, int NW>
+template <typename OT, bool MASK, int kSlots, int NW, bool BUF>
 __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int ntx,
                                                            const bf16_t* __restrict__ Q,
                                                            const bf16_t* __restrict__ K,
@@ -418,8 +418,22 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
     const char* zero = reinterpret_cast<const char*>(kBandZero);
     int tt0 = t.q0 - w + dr;                         // key of row dr of block 0
     uint32_t boff = (uint32_t)tt0 * row_bytes + dch * 16;   // used only when tt0 >= 0
+    // buffer form: byte offsets from the start of the residue subsequence; a key before
+    // it (negative offset, >= 2^31 as unsigned) or after it lies outside the buffer's
+    // range and reads zeros, so every block takes the same two loads per pass
+    const int nrec = (t.lr - 1) * (int)row_bytes + kD * 2;
+    const int voff0 = tt0 * (int)row_bytes + dch * 16;
     auto dma = [&](int kb) {
         u32x4* slot = lds + (kb % kSlots) * kSlotChunks;
+        if constexpr (BUF) {
+#pragma unroll
+            for (int e = 0; e < kPass; ++e) {
+                const uint32_t o2 = (uint32_t)(voff0 + (kb * kT + e * NW * 8) * (int)row_bytes);
+                buffer_copy16(kseq, nrec, o2, 0, (lds_void*)(slot + (e * NW + wv) * 64));
+                buffer_copy16(vseq, nrec, o2, 0, (lds_void*)(slot + 512 + (e * NW + wv) * 64));
+            }
+            return;
+        }
         const int tt = tt0 + kb * kT;
         const uint32_t off = boff + (uint32_t)(kb * kT) * row_bytes;
         if (t.q0 - w + kb * kT >= 0 && t.q0 - w + kb * kT + kT <= t.lr) {   // interior block
@@ -682,16 +696,23 @@ hipError_t launch_fused_nw(const BandGeom& g, const void* q, const void* k, cons
     const int64_t l0 = (g.l + g.dil - 1) / g.dil;
     const int ntx = (int)((l0 + 32 * NW - 1) / (32 * NW));
     const dim3 grid((unsigned)(ntx * g.dil * g.b));
-#define OLLIE_FUSED(OT, M)                                                                   \
-    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2, NW>), grid, dim3(64 * NW), 0, stream, g,  \
-                       ntx, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
+    // buffer-load copies need every key offset of a subsequence, including the band's
+    // reach before and after it, inside +-2^31 bytes
+    const bool buf = (l0 + g.w + 4 * kT) * g.dil * kD * 2 < (int64_t(1) << 31);
+#define OLLIE_FUSED(OT, M, B)                                                                \
+    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2, NW, B>), grid, dim3(64 * NW), 0, stream, \
+                       g, ntx, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
+#define OLLIE_FUSED_B(OT, M)            \
+    if (buf) OLLIE_FUSED(OT, M, true);  \
+    else OLLIE_FUSED(OT, M, false)
     if (o_bf16) {
-        if (mask) OLLIE_FUSED(bf16_t, true);
-        else OLLIE_FUSED(bf16_t, false);
+        if (mask) OLLIE_FUSED_B(bf16_t, true);
+        else OLLIE_FUSED_B(bf16_t, false);
     } else {
-        if (mask) OLLIE_FUSED(float, true);
-        else OLLIE_FUSED(float, false);
+        if (mask) OLLIE_FUSED_B(float, true);
+        else OLLIE_FUSED_B(float, false);
     }
+#undef OLLIE_FUSED_B
 #undef OLLIE_FUSED
     return hipGetLastError();
 }

@@ -117,6 +117,17 @@ __device__ __forceinline__ int tile_swz_k(int row, int ch) {
     else return row * 4 + (ch ^ ((row >> 1) & 3));
 }
 
+// One 16-byte-per-lane copy global->LDS through a raw buffer load: lane L's chunk at
+// byte offset voff + soff of `base` lands at dst + 16 L.  An offset at or beyond
+// `nbytes` reads zeros.  (Kept out of templates: the buffer-resource type inside a
+// kernel template stops the host pass from emitting that kernel's launch stub.)
+__device__ __forceinline__ void buffer_copy16(const void* base, int nbytes, uint32_t voff,
+                                              int soff, lds_void* dst) {
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, 0x00020000);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+}
+
 // s_waitcnt with only the vector-memory counter constrained (expcnt, lgkmcnt at max).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {

@@ -78,17 +78,6 @@ __device__ __forceinline__ TileId tile_of(const FusedPlan& P, int bm, int bn) {
     return t;
 }
 
-// One 16-byte-per-lane copy global->LDS through a raw buffer load: lane L's chunk at
-// byte offset voff + soff of `base` lands at dst + 16 L.  An offset at or beyond
-// `nbytes` reads zeros.  (Kept out of templates: the buffer-resource type inside a
-// kernel template stops the host pass from emitting that kernel's launch stub.)
-__device__ __forceinline__ void buffer_copy16(const void* base, int nbytes, uint32_t voff,
-                                              int soff, lds_void* dst) {
-    const __amdgpu_buffer_rsrc_t r =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, nbytes, 0x00020000);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
-}
-
 // Global->LDS copies of one k-tile (64 channels) of the operand tiles: BM rows of X
 // gathered through the class's index map and BN rows of Wt, 16-byte chunks written to
 // the XOR-swizzled LDS layout (the swizzle is applied to the source chunk, since one
@@ -117,6 +106,7 @@ struct TileCopy {
     int wrow[B];                     // output channel of each Wt row
     AxisTaps th, tw;                 // the class's taps
     int ri, si, kc;                  // k-tile the next issue() copies: tap (ri, si), channels kc
+    int left;                        // k-tiles not yet copied (the last one repeats after)
     int bh, bw, rs;
 
     __device__ __forceinline__ void init(const FusedPlan& P, const TileId& t, const bf16_t* x,
@@ -147,6 +137,7 @@ struct TileCopy {
         }
         th = P.cls_th[t.cls]; tw = P.cls_tw[t.cls];
         ri = 0; si = 0; kc = 0;
+        left = th.n * tw.n * kc_n;
         set_tap(P);
     }
     // tap quantities from scalar arithmetic (no table reads inside the main loop)
@@ -164,8 +155,14 @@ struct TileCopy {
             }
         }
     }
-    // copies the next k-tile into `slot` and advances to the one after it
+    // copies the current k-tile into `slot` and advances to the next one; past the last
+    // k-tile it copies the last one again (the callers issue a fixed number of copies
+    // per iteration, so the copy counters need no branches)
     __device__ __forceinline__ void issue(const FusedPlan& P, u32x4* slot) {
+        copy(slot);
+        advance(P);
+    }
+    __device__ __forceinline__ void copy(u32x4* slot) {
         if constexpr (BUF) {
             const int kofs = kc * kTileK * 2;
             const int wsoff = rs * K * C * 2 + kofs;
@@ -195,6 +192,10 @@ struct TileCopy {
                     (const void*)(Wt + ((int64_t)rs * K + wrow[i]) * C + kc * kTileK + cho),
                     (lds_void*)(slot + BM * kTileChunks + (i * NW + wave) * 64), 16, 0, 0);
         }
+    }
+    // moves to the next k-tile (the last one stays current once reached)
+    __device__ __forceinline__ void advance(const FusedPlan& P) {
+        if (--left <= 0) return;
         if (++kc == kc_n) {
             kc = 0;
             if (++si == tw.n) {
@@ -271,14 +272,14 @@ void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ 
 #pragma unroll
         for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
+    // every iteration issues one k-tile of copies (repeats of the last one near the end
+    // land in slots nobody reads again), so the copy counter waits are constant
 #pragma unroll
-    for (int s = 0; s < NSTAGE - 1; ++s)
-        if (s < total) cp.issue(P, lds + s * STAGE_CHUNKS);
+    for (int s = 0; s < NSTAGE - 1; ++s) cp.issue(P, lds + s * STAGE_CHUNKS);
     for (int it = 0; it < total; ++it) {
-        if (it + NSTAGE - 2 < total) wait_vmcnt<(NSTAGE - 2) * LOADS>();
-        else wait_vmcnt<0>();
+        wait_vmcnt<(NSTAGE - 2) * LOADS>();
         __builtin_amdgcn_s_barrier();   // tile `it` is in LDS everywhere; `it - 1` is consumed
-        if (it + NSTAGE - 1 < total) cp.issue(P, lds + ((it + NSTAGE - 1) % NSTAGE) * STAGE_CHUNKS);
+        cp.copy(lds + ((it + NSTAGE - 1) % NSTAGE) * STAGE_CHUNKS);
         const u32x4* la = lds + (it % NSTAGE) * STAGE_CHUNKS;
         const u32x4* lb = la + BM * kTileChunks;
 #pragma unroll
@@ -300,7 +301,9 @@ void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ 
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j],
                                                                         0, 0, 0);
         }
+        cp.advance(P);
     }
+    wait_vmcnt<0>();   // no copy into LDS may still be in flight when the workgroup ends
     store_tile<FM, FN, WM, WN, OT>(P, t, wm, wn, acc, out, epi);
 }
 
@@ -361,11 +364,11 @@ void conv_fused_pipe_kernel(const bf16_t* __restrict__ X, const bf16_t* __restri
                                                                     0, 0, 0);
     };
 
+    // one k-tile of copies per iteration, repeats of the last k-tile near the end (into
+    // slots nobody reads again), so the copy counter waits are constant
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-        if (s < total) cp.issue(P, lds + s * STAGE_CHUNKS);
-    if (total >= NS) wait_vmcnt<(NS - 1) * LOADS>();
-    else wait_vmcnt<0>();
+    for (int s = 0; s < NS; ++s) cp.issue(P, lds + s * STAGE_CHUNKS);
+    wait_vmcnt<(NS - 1) * LOADS>();
     __builtin_amdgcn_s_barrier();
     Frag F, G;
     read(0, 0, F);
@@ -377,21 +380,30 @@ void conv_fused_pipe_kernel(const bf16_t* __restrict__ X, const bf16_t* __restri
         __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
         // before k-tile it+1 is read: its copies have landed (only those of the later
         // k-tiles may still be in flight), and this wave's reads of slot it are done
-        if (it + NS - 1 < total) wait_vmcnt<(NS - 2) * LOADS>();
-        else wait_vmcnt<0>();
+        __builtin_amdgcn_sched_barrier(0);    // nothing moves across the barrier
+        wait_vmcnt<(NS - 2) * LOADS>();
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
         __builtin_amdgcn_s_barrier();
-        if (it + NS < total) cp.issue(P, lds + (it % NS) * STAGE_CHUNKS);
+        __builtin_amdgcn_sched_barrier(0);
+        cp.copy(lds + (it % NS) * STAGE_CHUNKS);
         read(it + 1, 0, F);
         mma(G);
+        // reads of F first, then the copies spread between the MFMAs on G
         __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, (FM * FN) / LOADS, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - ((FM * FN) / LOADS) * LOADS, 0);
+        cp.advance(P);
     }
-    if (total > 0) {   // the last k-tile: no copies or reads of a next one
+    if (total > 0) {   // the last k-tile: no reads of a next one
         read(total - 1, 1, G);
         mma(F);
         mma(G);
     }
+    wait_vmcnt<0>();   // no copy into LDS may still be in flight when the workgroup ends
     store_tile<FM, FN, WM, WN, OT>(P, t, wm, wn, acc, out, epi);
 }
 
