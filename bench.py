@@ -39,7 +39,9 @@ PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 # derived-program variant per convolution workload: "staged" = GEMM stage + eOperator
-# through the Y scope, "fused" = the fused expression (no Y)
+# through the Y scope, "fused" = the fused expression (no Y), "residues" = the fused
+# expression of the dilated convolution as non-dilated convolutions over its residue
+# sub-images (the dilated workload only)
 PATHS = {2: "fused", 3: "fused", 4: "fused"}
 
 
@@ -102,6 +104,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--stage", default=None, help="launch only this stage kernel")
+    ap.add_argument("--dilated-path", default=None, choices=["staged", "fused", "residues"],
+                    help="derived-program variant of the dilated workload (default: PATHS)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this library has no multi-GPU path "
@@ -131,13 +135,17 @@ def main():
         ws = torch.empty(ol.conv_workspace_bytes(desc, wl.transposed), dtype=torch.uint8,
                          device=dev)
         kw = dict(stride=wl.stride, padding=wl.pad, out=out, ws=ws)
-        fused = PATHS[cfg] == "fused"
+        path = PATHS[cfg] if cfg != 4 or not args.dilated_path else args.dilated_path
+        fused = path != "staged"
+        if path == "residues":
+            kw["residues"] = True
         if cfg == 3:
             kw["output_padding"] = wl.out_pad
         if cfg == 4:
             kw["dilation"] = wl.dil
         flops, eop_bytes = conv_costs(wl, ho, wo)
         conv_ops.append(dict(cfg=cfg, wl=wl, entry=entry, x=x, wt=wt, kw=kw, desc=desc, ws=ws,
+                             path=path,
                              out=out, flops=flops, eop_bytes=eop_bytes, fused=fused,
                              m=wl.n * wl.h * wl.w, nc=wl.r * wl.s * wl.k))
     bwl = synth.WORKLOADS[5]
@@ -216,20 +224,23 @@ def main():
         g_ms = time_kernel(lambda: ol.gemm_nt(a, b, out=y), reps)
         e_ms = time_kernel(lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y,
                                                  out=op["out"]), reps)
+        kw_f = {k_: v_ for k_, v_ in op["kw"].items() if k_ != "residues"}
         f_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
-                                               **dict(op["kw"], ws=None, fuse=True)), reps)
+                                               **dict(kw_f, ws=None, fuse=True)), reps)
         r_ms = None
         if op["cfg"] == 4:   # the dilated workload also in the residue sub-image form
             r_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
-                                                   **dict(op["kw"], ws=None, residues=True)),
+                                                   **dict(kw_f, ws=None, residues=True)),
                                reps)
+        k_ms = r_ms if op["path"] == "residues" else f_ms   # the fused kernel the step runs
+        k_tf = op["flops"] / (k_ms * 1e-3) / 1e12
         g_tf = op["flops"] / (g_ms * 1e-3) / 1e12
         e_gb = op["eop_bytes"] / (e_ms * 1e-3) / 1e9
         f_tf = op["flops"] / (f_ms * 1e-3) / 1e12
         name = op["wl"].name
         per_cfg[name] = {
-            "path": PATHS[op["cfg"]],
-            "op_ms": round(f_ms if op["fused"] else g_ms + e_ms, 5),
+            "path": op["path"],
+            "op_ms": round(k_ms if op["fused"] else g_ms + e_ms, 5),
             "gemm_ms": round(g_ms, 5), "gemm_tflops": round(g_tf, 2),
             "gemm_pct_mfma_peak": round(100 * g_tf / PEAK_BF16_TFLOPS, 2),
             "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
@@ -241,7 +252,7 @@ def main():
         if r_ms is not None:
             per_cfg[name]["fused_residue_form_ms"] = round(r_ms, 5)
         if op["fused"]:
-            kernels.append((f"conv_fused[{name}]", f_ms, "mfma", f_tf, PEAK_BF16_TFLOPS,
+            kernels.append((f"conv_fused[{name}]", k_ms, "mfma", k_tf, PEAK_BF16_TFLOPS,
                             "TFLOP/s", op["flops"]))
         else:
             kernels.append((f"gemm_nt[{name}]", g_ms, "mfma", g_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
@@ -277,7 +288,7 @@ def main():
                                "8x8) + dilated conv3x3 d2 (C512 96x128) + band (B96 L4096 d64 "
                                "w256 dil2), bf16 in, fp32 accumulate/out",
                    "parallelism": "single GPU", "launch": "stream",
-                   "paths": {synth.WORKLOADS[c].name: p for c, p in PATHS.items()}},
+                   "paths": {op["wl"].name: op["path"] for op in conv_ops}},
         "per_config": per_cfg,
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -407,6 +407,150 @@ void conv_fused_pipe_kernel(const bf16_t* __restrict__ X, const bf16_t* __restri
     store_tile<FM, FN, WM, WN, OT>(P, t, wm, wn, acc, out, epi);
 }
 
+// Row-window form for classes whose taps along w step by one class column (the residue
+// form, and stride-1 undilated convolutions): the A operand of the taps (r, s) of one
+// kernel row r is, for every s, the same window of input rows shifted by s columns.
+// So a k-tile stage covers one (kernel row r, 64 channels) pair: the window of the
+// tile's class rows, TH rows of (wc + S - 1) input pixels, is copied once and read at
+// column offsets s = 0..S-1 by the MFMA fragments, next to the S weight slices of that
+// kernel row.  Against per-tap copies of the 192 gathered rows this moves 40% fewer
+// bytes from L2 per MFMA, which is what bounds the large dilated layer.
+//
+// Fixed shape: 192 x 128 output tile, 8 waves (2 x 4, each 96 x 32), two 80 KB stages
+// (one workgroup per CU).  Needs wc % 16 == 0 (a 16-pixel MFMA fragment stays in one
+// class row), 192 % wc == 0 (the tile is TH = 192 / wc whole class rows; a tile may
+// straddle two images) and S <= 3.  The sum runs over taps in the order (r, channels,
+// s), a different summation order from the per-tap forms.
+constexpr int kWinBM = 192, kWinBN = 128, kWinArows = 256, kWinS = 3;
+
+template <typename OT>
+__global__ __launch_bounds__(512, 1)
+void conv_window_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+                        OT* __restrict__ out, FusedPlan P, Epi epi) {
+    constexpr int NW = 8, BM = kWinBM, BN = kWinBN;
+    constexpr int WM = BM / 2, WN = BN / 4, FM = WM / 16, FN = WN / 16;
+    constexpr int A_CHUNKS = kWinArows * kTileChunks;
+    constexpr int STAGE_CHUNKS = A_CHUNKS + kWinS * BN * kTileChunks;
+    constexpr int A_MAX = kWinArows / (8 * NW);          // window copy instructions per wave
+    constexpr int B_LOADS = kWinS * BN / (8 * NW);       // weight copy instructions per wave
+    __shared__ u32x4 lds[2 * STAGE_CHUNKS];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave / 4, wn = wave % 4;
+    const TileId t = tile_of(P, BM, BN);
+    const AxisTaps th = P.cls_th[t.cls], tw = P.cls_tw[t.cls];
+    const int ns = tw.n;                       // taps along w (1..3)
+    const int wrow = t.wc + ns - 1;            // window row length (input pixels)
+    const int thr = BM / t.wc;                 // class rows per tile
+    const int g0 = t.m0 / t.wc;                // first class row (over images)
+    const int hc = t.plane / t.wc;
+    const int nrows = P.n * hc;                // class rows over all images
+    const int H = P.h, W = P.w, C = P.c, K = P.k;
+    const int kc_n = C / kTileK;
+    const int total = th.n * kc_n;
+    const int nA = (thr * wrow + 7) / 8;       // window copy instructions in all
+    const int cho = ((lane & 7) ^ ((lane >> 3) & 7)) * 8;
+
+    // window rows of this lane: input pixel base (tap row 0) and its validity
+    int wpix[A_MAX], whi[A_MAX], wwi[A_MAX];
+#pragma unroll
+    for (int i = 0; i < A_MAX; ++i) {
+        const int q = (i * NW + wave) * 8 + (lane >> 3);
+        const int ii = q / wrow, jj = q - ii * wrow;
+        const int g = g0 + ii;
+        const int nn = g / hc, ci = g - nn * hc;
+        const bool rowok = ii < thr && g < nrows;
+        whi[i] = rowok ? P.alpha_h * ci + th.b0 : -(1 << 28);
+        wwi[i] = P.alpha_w * jj + tw.b0;
+        wpix[i] = rowok ? (nn * H + whi[i]) * W + wwi[i] : 0;
+    }
+    // weight rows of this lane: slice s = q / BN, output channel k0 + q % BN
+    int wofs[B_LOADS];
+#pragma unroll
+    for (int i = 0; i < B_LOADS; ++i) {
+        const int q = (i * NW + wave) * 8 + (lane >> 3);
+        int kk = t.k0 + q % BN;
+        kk = kk < K ? kk : K - 1;
+        wofs[i] = (kk * C + cho) * 2;
+    }
+    // fragment rows: output pixel m' = wm*WM + j*16 + lane%16 of the tile sits at window
+    // row (m' / wc) * wrow + m' % wc for s = 0
+    int arow[FM];
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+        const int mm = wm * WM + j * 16 + (lane & 15);
+        arow[j] = (mm / t.wc) * wrow + mm % t.wc;
+    }
+
+    uint32_t wv[A_MAX];      // window offsets of the current kernel row
+    int cur_r = -1;
+    auto copy = [&](int stage, u32x4* slot) {
+        const int r = stage / kc_n, kc = stage - r * kc_n;
+        if (r != cur_r) {
+            cur_r = r;
+            const int dh = r * th.bstep;
+#pragma unroll
+            for (int i = 0; i < A_MAX; ++i) {
+                const bool ok = (unsigned)(whi[i] + dh) < (unsigned)H &&
+                                (unsigned)wwi[i] < (unsigned)W;
+                wv[i] = ok ? (uint32_t)(((wpix[i] + dh * W) * C + cho) * 2) : 0x80000000u;
+            }
+        }
+        const int kofs = kc * kTileK * 2;
+#pragma unroll
+        for (int i = 0; i < A_MAX; ++i)
+            if (i * NW + wave < nA)
+                buffer_copy16(X, P.x_bytes, wv[i] + kofs, 0,
+                              (lds_void*)(slot + (i * NW + wave) * 64));
+        const int rk = th.r0 + r * th.rstep;
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+            const int sl = ((i * NW + wave) * 8) / BN;           // weight slice (uniform)
+            const int s2 = sl < ns ? sl : ns - 1;
+            const int rs = rk * P.s + tw.r0 + s2 * tw.rstep;
+            buffer_copy16(Wt, P.w_bytes, wofs[i], rs * K * C * 2 + kofs,
+                          (lds_void*)(slot + A_CHUNKS + (i * NW + wave) * 64));
+        }
+    };
+
+    f32x4 acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+
+    if (total > 0) copy(0, lds);
+    for (int it = 0; it < total; ++it) {
+        wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();   // stage `it` is in LDS everywhere; `it - 1` is consumed
+        if (it + 1 < total) copy(it + 1, lds + ((it + 1) & 1) * STAGE_CHUNKS);
+        const u32x4* la = lds + (it & 1) * STAGE_CHUNKS;
+        const u32x4* lb = la + A_CHUNKS;
+        for (int sl = 0; sl < ns; ++sl) {
+#pragma unroll
+            for (int kk = 0; kk < kTileK / 32; ++kk) {
+                const int ch = kk * 4 + (lane >> 4);
+                bf16x8 fa[FN], fb[FM];
+#pragma unroll
+                for (int i = 0; i < FN; ++i)
+                    fa[i] = __builtin_bit_cast(
+                        bf16x8, lb[tile_swz(sl * BN + wn * WN + i * 16 + (lane & 15), ch)]);
+#pragma unroll
+                for (int j = 0; j < FM; ++j)
+                    fb[j] = __builtin_bit_cast(bf16x8, la[tile_swz(arow[j] + sl, ch)]);
+#pragma unroll
+                for (int i = 0; i < FN; ++i)
+#pragma unroll
+                    for (int j = 0; j < FM; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j],
+                                                                            acc[i][j], 0, 0, 0);
+            }
+        }
+    }
+    store_tile<FM, FN, WM, WN, OT>(P, t, wm, wn, acc, out, epi);
+}
+
 // Host-side plan: classes, their taps, and the tile count for a BM x BN tiling.
 //
 // Taps along one axis of a class, as (kernel index, input offset) pairs in increasing
@@ -516,23 +660,49 @@ hipError_t go_pipe(FusedPlan& P, const void* x, const void* wt, void* out, const
     return hipGetLastError();
 }
 
+// Whether every class fits the row-window kernel.
+bool window_ok(const FusedPlan& P) {
+    for (int c = 0; c < P.ncls; ++c) {
+        const AxisTaps& tw = P.cls_tw[c];
+        const int wc = P.cls_wc[c];
+        if (wc % 16 != 0 || kWinBM % wc != 0 || tw.n < 1 || tw.n > kWinS) return false;
+        if (tw.n > 1 && tw.bstep != P.alpha_w) return false;
+        if ((kWinBM / wc) * (wc + tw.n - 1) > kWinArows) return false;
+    }
+    return true;
+}
+
+template <typename OT>
+hipError_t go_window(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
+                     hipStream_t st) {
+    const int64_t tiles = plan_tiles(P, kWinBM, kWinBN);
+    if (tiles == 0) return hipSuccess;
+    hipLaunchKernelGGL((conv_window_kernel<OT>), dim3((unsigned)tiles), dim3(512), 0, st,
+                       (const bf16_t*)x, (const bf16_t*)wt, (OT*)out, P, epi);
+    return hipGetLastError();
+}
+
 // Tile shapes: 0 = 192x128 with 8 waves (one workgroup per CU), 1 = 128x128 with 8 waves
 // (two per CU), 2 = 64x128 with 4 waves, 3 = 64x64 with 8 waves and a 4-stage copy ring;
 // 4-8 = the software-pipelined four-wave form with 192x128, 128x128, 64x64, 128x64 and
-// 256x128 tiles.  The first of 0, 1, 2 with at least ~one tile per CU is taken, else 6
-// (the small convolutions: measured fastest of all nine on the ResNet and DCGAN layers).
-// OLLIE_FUSED_CONFIG overrides the choice for tuning sweeps.
+// 256x128 tiles; 9 = the row-window kernel (192x128).  The first of 0, 1, 2 with at least
+// ~one tile per CU is taken, else 6 (the small convolutions: measured fastest of all on
+// the ResNet and DCGAN layers).  The row-window kernel copies 35% fewer bytes on the
+// CSRNet layer in the residue form but measured no faster than 0 there (its copies
+// overlap less with the MFMA work), so it is selected only on request.
+// OLLIE_FUSED_CONFIG overrides the choice (tuning sweeps, tests); 9 falls back to the
+// automatic choice where the row-window form does not apply.
 template <typename OT>
 hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
                     hipStream_t st) {
-    static const int forced = [] {
-        const char* e = getenv("OLLIE_FUSED_CONFIG");
-        return e ? atoi(e) : -1;
-    }();
+    // read per call, so that a process can switch tile shapes between calls
+    const char* env = getenv("OLLIE_FUSED_CONFIG");
+    const int forced = env ? atoi(env) : -1;
     // tensors of 2 GiB or more: 64-bit addressing (buffer offsets are 32-bit)
     if (P.x_bytes == 0 || P.w_bytes == 0) return go<128, 128, 2, OT, 8, false>(P, x, wt, out, epi, st);
     int cfg = forced;
-    if (cfg < 0 || cfg > 8) {
+    if (cfg == 9 && !window_ok(P)) cfg = -1;
+    if (cfg < 0 || cfg > 9) {
         FusedPlan tmp = P;
         if (plan_tiles(tmp, 192, 128) >= 240) cfg = 0;
         else if (plan_tiles(tmp, 128, 128) >= 240) cfg = 1;
@@ -549,6 +719,7 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
     case 6: return go_pipe<64, 64, 4, OT>(P, x, wt, out, epi, st);
     case 7: return go_pipe<128, 64, 4, OT>(P, x, wt, out, epi, st);
     case 8: return go_pipe<256, 128, 3, OT>(P, x, wt, out, epi, st);
+    case 9: return go_window<OT>(P, x, wt, out, epi, st);
     // the small shapes run right after other kernels have evicted their operands: a
     // 4-deep copy ring hides the longer cold loads (measured in the benchmark step)
     default: return go_pipe<64, 64, 4, OT>(P, x, wt, out, epi, st);

@@ -448,6 +448,40 @@ def test_small_shapes_fused(ci, integer):
         assert err(to_np(out), ref) <= TOL_BF16
 
 
+# Every tile shape of the fused expression (OLLIE_FUSED_CONFIG 0-9, read per call), on
+# shapes that exercise the row-window kernel (config 9: stride-1 forms whose class width
+# is a multiple of 16 dividing 192 -- ragged channel tiles, tiles straddling images,
+# kernel widths 1-3) and on shapes where config 9 falls back to the automatic choice.
+TILE_CASES = [
+    # kind, n, c, h, w, k, r, s, stride, pad, dil, out_pad, residues
+    ("conv2d", 2, 128, 9, 32, 72, 3, 3, (1, 1), (1, 1), (1, 1), (0, 0), False),
+    ("dilated_conv2d", 1, 64, 13, 64, 40, 3, 3, (1, 1), (2, 2), (2, 2), (0, 0), True),
+    ("dilated_conv2d", 1, 64, 10, 96, 24, 3, 2, (1, 1), (1, 1), (2, 2), (0, 0), True),
+    ("conv2d", 1, 64, 6, 16, 20, 1, 1, (1, 1), (0, 0), (1, 1), (0, 0), False),
+    ("conv_transpose2d", 2, 64, 5, 6, 12, 4, 4, (2, 2), (1, 1), (1, 1), (1, 0), False),
+    ("dilated_conv2d", 1, 64, 8, 32, 130, 3, 3, (1, 1), (2, 2), (2, 2), (0, 0), False),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(TILE_CASES)))
+@pytest.mark.parametrize("cfg", range(10))
+def test_every_tile_shape_integer_exact(cfg, ci, monkeypatch):
+    kind, n, c, h, w, k, r, s, st, pd, dl, op, res = TILE_CASES[ci]
+    say("tile shape", cfg, TILE_CASES[ci])
+    monkeypatch.setenv("OLLIE_FUSED_CONFIG", str(cfg))
+    x = synth.random_tensor((n, h, w, c), 36000 + ci, "bf16", integer=True)
+    wt = synth.random_tensor((r, s, k, c), 36100 + ci, "bf16", integer=True)
+    xg, wg = x.to(DEV), wt.to(DEV)
+    if kind == "conv2d":
+        out = ol.derived_conv2d(xg, wg, st, pd, fuse=True)
+    elif kind == "dilated_conv2d":
+        out = ol.derived_dilated_conv2d(xg, wg, st, pd, dl, fuse=True, residues=res)
+    else:
+        out = ol.derived_conv_transpose2d(xg, wg, st, pd, op, dl, fuse=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out), oracle_conv(kind, x, wt, st, pd, dl, op))
+
+
 def test_fused_flag_falls_back_to_two_stages():
     """c % 64 != 0: the fused kernel does not cover the shape, the call takes the
     two-stage path (and needs its workspace)."""
