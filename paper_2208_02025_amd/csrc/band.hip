@@ -352,8 +352,8 @@ __device__ __forceinline__ void block_sync() {
     asm volatile("" ::: "memory");
 }
 
-template <typename OT, bool MASK, int kSlots, int NW, bool BUF>
-__global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int ntx,
+template <typename OT, bool MASK, int kSlots, int NW, bool BUF, int HQ>
+__global__ __launch_bounds__(64 * NW, HQ <= 2 ? 4 : 2) void band_fused_kernel(BandGeom g, int ntx,
                                                            const bf16_t* __restrict__ Q,
                                                            const bf16_t* __restrict__ K,
                                                            const bf16_t* __restrict__ V,
@@ -363,7 +363,7 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
     // the fp32 range, and bf16 p keeps its relative precision at any magnitude.  A wide
     // margin means the reference settles after the first block and rescaling is rare.
     constexpr float kLazy = 64.f;
-    constexpr int kQW = 32;               // queries per wave
+    constexpr int kQW = 16 * HQ;          // queries per wave (HQ groups of 16)
     constexpr int kFT = NW * kQW;         // queries per tile (NW waves)
     constexpr int kPass = 64 / (NW * 8);  // copy instructions per lane per 64-row block
     __shared__ u32x4 lds[kSlots * kSlotChunks];
@@ -389,9 +389,9 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
     const float sl2 = fmaxf(fabsf(g.scale) * 1.4426950408889634f, 1.17549435e-38f);
     const uint32_t qflip = g.scale < 0.f ? 0x80008000u : 0u;
 
-    bf16x8 qf[2][2];
+    bf16x8 qf[HQ][2];
 #pragma unroll
-    for (int hq = 0; hq < 2; ++hq) {
+    for (int hq = 0; hq < HQ; ++hq) {
         const int q = qa + hq * 16 + li;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -488,10 +488,10 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
         else wait_vmcnt<0>();
     };
 
-    f32x4 o[2][4], lsum[2];
-    float m_run[2];
+    f32x4 o[HQ][4], lsum[HQ];
+    float m_run[HQ];
 #pragma unroll
-    for (int hq = 0; hq < 2; ++hq) {
+    for (int hq = 0; hq < HQ; ++hq) {
         lsum[hq] = (f32x4){0.f, 0.f, 0.f, 0.f};
         m_run[hq] = -INFINITY;
 #pragma unroll
@@ -508,11 +508,11 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
             for (int kk = 0; kk < 2; ++kk)
                 kf[ft][kk] = *reinterpret_cast<const bf16x8*>(sb + koff[kk] + ft * 16 * 128);
     };
-    auto scores = [&](const bf16x8 (&kf)[4][2], f32x4 (&s)[2][4]) {
+    auto scores = [&](const bf16x8 (&kf)[4][2], f32x4 (&s)[HQ][4]) {
 #pragma unroll
         for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
-            for (int hq = 0; hq < 2; ++hq) {
+            for (int hq = 0; hq < HQ; ++hq) {
                 f32x4 acc = {0.f, 0.f, 0.f, 0.f};
                 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][0], qf[hq][0], acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ft][1], qf[hq][1], acc, 0, 0, 0);
@@ -523,7 +523,7 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
     // One block iteration: scores, softmax and P*V of block kb.
     auto step = [&](int kb) {
         const int t0 = t.q0 - w + kb * kT;
-        f32x4 s[2][4];
+        f32x4 s[HQ][4];
         {
             bf16x8 kf[4][2];
             read_k(kb, kf);
@@ -533,7 +533,7 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
         if (MASK) full = full && t0 >= 0 && t0 + kT <= t.lr;
         if (!full) {                               // band (and range) mask, in place
 #pragma unroll
-            for (int hq = 0; hq < 2; ++hq) {
+            for (int hq = 0; hq < HQ; ++hq) {
                 const int base = t0 + 4 * grp - (qa + hq * 16 + li) + w;
 #pragma unroll
                 for (int ft = 0; ft < 4; ++ft)
@@ -548,9 +548,9 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
                     }
             }
         }
-        float mb[2];
+        float mb[HQ];
 #pragma unroll
-        for (int hq = 0; hq < 2; ++hq) {
+        for (int hq = 0; hq < HQ; ++hq) {
             mb[hq] = -INFINITY;
 #pragma unroll
             for (int ft = 0; ft < 4; ++ft)
@@ -558,9 +558,12 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
                 for (int v = 0; v < 4; ++v) mb[hq] = fmaxf(mb[hq], s[hq][ft][v]);
         }
         // lazy reference update; the row maximum (4 lanes) only when a lane asks for it
-        if (__any(mb[0] * sl2 > m_run[0] + kLazy || mb[1] * sl2 > m_run[1] + kLazy)) {
+        bool up = false;
 #pragma unroll
-            for (int hq = 0; hq < 2; ++hq) {
+        for (int hq = 0; hq < HQ; ++hq) up = up || mb[hq] * sl2 > m_run[hq] + kLazy;
+        if (__any(up)) {
+#pragma unroll
+            for (int hq = 0; hq < HQ; ++hq) {
                 float m = mb[hq];
                 m = fmaxf(m, __int_as_float(__builtin_amdgcn_ds_bpermute(xor16, __float_as_int(m))));
                 m = fmaxf(m, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32, __float_as_int(m))));
@@ -574,9 +577,9 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
                 m_run[hq] = m_new;
             }
         }
-        bf16x8 pf[2][2];
+        bf16x8 pf[HQ][2];
 #pragma unroll
-        for (int hq = 0; hq < 2; ++hq) {
+        for (int hq = 0; hq < HQ; ++hq) {
             const float nm = m_run[hq] == -INFINITY ? 0.f : -m_run[hq];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
@@ -605,11 +608,11 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
 #pragma unroll
             for (int eb = 0; eb < 4; ++eb)
 #pragma unroll
-                for (int hq = 0; hq < 2; ++hq)
+                for (int hq = 0; hq < HQ; ++hq)
                     o[hq][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[eb], pf[hq][h],
                                                                         o[hq][eb], 0, 0, 0);
 #pragma unroll
-            for (int hq = 0; hq < 2; ++hq)
+            for (int hq = 0; hq < HQ; ++hq)
                 lsum[hq] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[hq][h], lsum[hq],
                                                                    0, 0, 0);
         }
@@ -629,7 +632,7 @@ __global__ __launch_bounds__(64 * NW, 4) void band_fused_kernel(BandGeom g, int 
         block_sync();
     }
 #pragma unroll
-    for (int hq = 0; hq < 2; ++hq) {
+    for (int hq = 0; hq < HQ; ++hq) {
         const int q = qa + hq * 16 + li;
         if (q >= t.lr) continue;
         const float inv = 1.f / lsum[hq][0];
@@ -690,17 +693,17 @@ hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, voi
     return hipGetLastError();
 }
 
-template <int NW>
+template <int NW, int HQ>
 hipError_t launch_fused_nw(const BandGeom& g, const void* q, const void* k, const void* v,
                            void* o, int o_bf16, int mask, hipStream_t stream) {
     const int64_t l0 = (g.l + g.dil - 1) / g.dil;
-    const int ntx = (int)((l0 + 32 * NW - 1) / (32 * NW));
+    const int ntx = (int)((l0 + 16 * HQ * NW - 1) / (16 * HQ * NW));
     const dim3 grid((unsigned)(ntx * g.dil * g.b));
     // buffer-load copies need every key offset of a subsequence, including the band's
     // reach before and after it, inside +-2^31 bytes
     const bool buf = (l0 + g.w + 4 * kT) * g.dil * kD * 2 < (int64_t(1) << 31);
 #define OLLIE_FUSED(OT, M, B)                                                                \
-    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2, NW, B>), grid, dim3(64 * NW), 0, stream, \
+    hipLaunchKernelGGL((band_fused_kernel<OT, M, 2, NW, B, HQ>), grid, dim3(64 * NW), 0, stream, \
                        g, ntx, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
 #define OLLIE_FUSED_B(OT, M)            \
     if (buf) OLLIE_FUSED(OT, M, true);  \
@@ -717,11 +720,18 @@ hipError_t launch_fused_nw(const BandGeom& g, const void* q, const void* k, cons
     return hipGetLastError();
 }
 
-// Four waves per workgroup: measured faster than eight (half the copies per query, but
-// the same occupancy and twice the LDS per workgroup).
+// Wave shapes: 0 = four waves of 32 queries (the default: measured faster than eight
+// waves, which have half the copies per query but the same occupancy and twice the LDS
+// per workgroup), 1 = four waves of 64 queries, 2 = two waves of 64 queries (half the
+// LDS reads per score, two waves per SIMD).  OLLIE_BAND_CONFIG overrides the choice
+// (read per call; sweeps and tests).
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
                              void* o, int o_bf16, int mask, hipStream_t stream) {
-    return launch_fused_nw<4>(g, q, k, v, o, o_bf16, mask, stream);
+    const char* env = getenv("OLLIE_BAND_CONFIG");
+    const int cfg = env ? atoi(env) : 0;
+    if (cfg == 1) return launch_fused_nw<4, 4>(g, q, k, v, o, o_bf16, mask, stream);
+    if (cfg == 2) return launch_fused_nw<2, 4>(g, q, k, v, o, o_bf16, mask, stream);
+    return launch_fused_nw<4, 2>(g, q, k, v, o, o_bf16, mask, stream);
 }
 
 }  // namespace ollie

@@ -243,24 +243,34 @@ __device__ __forceinline__ void store_tile(const FusedPlan& P, const TileId& t, 
     }
 }
 
-// NW = 4 or 8 waves (2 x NW/2 over the tile), several workgroups per CU.  Eight waves
-// keep twice as many global->LDS copies in flight per workgroup, which is what bounds
-// the small shapes.
-template <int BM, int BN, int NSTAGE, typename OT, int NW, bool BUF>
+// NW = 4 or 8 waves over the tile, several workgroups per CU.  Eight waves keep twice
+// as many global->LDS copies in flight per workgroup, which is what bounds the small
+// shapes.  KS = 1: the waves tile the output 2 x NW/2.  KS = 2: the two halves of the
+// waves take the two 32-deep halves of every k-tile over the same 2 x NW/4 output
+// tiling, and the halves' accumulators are summed through LDS at the end; per MFMA the
+// larger wave blocks read 3/8 fewer LDS bytes, at two waves per SIMD.
+template <int BM, int BN, int NSTAGE, typename OT, int NW, bool BUF, int KS = 1>
 __global__ __launch_bounds__(64 * NW, NSTAGE * (BM + BN) * kTileChunks * 16 <= 80 * 1024 ? 2 : 1)
 void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
                        OT* __restrict__ out, FusedPlan P, Epi epi) {
-    constexpr int WM = BM / 2, WN = BN / (NW / 2);
+    static_assert(KS == 1 || KS == 2, "k split");
+    constexpr int NWO = NW / KS;                 // waves over the output tile
+    constexpr int WM = BM / 2, WN = BN / (NWO / 2);
     constexpr int FM = WM / 16, FN = WN / 16;
     constexpr int STAGE_CHUNKS = (BM + BN) * kTileChunks;
+    constexpr int RED_CHUNKS = KS == 2 ? NWO * FN * FM * 64 : 0;   // f32x4 partial sums
+    constexpr int LDS_CHUNKS =
+        NSTAGE * STAGE_CHUNKS > RED_CHUNKS ? NSTAGE * STAGE_CHUNKS : RED_CHUNKS;
     using Copy = TileCopy<NW, BM, BN, BUF>;
     constexpr int LOADS = Copy::LOADS;
     static_assert(FM >= 1 && FN >= 1, "wave tile");
-    __shared__ u32x4 lds[NSTAGE * STAGE_CHUNKS];
+    __shared__ u32x4 lds[LDS_CHUNKS];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int wm = wave / (NW / 2), wn = wave % (NW / 2);
+    const int kh = wave / NWO;                   // k half (KS = 2)
+    const int wo = wave % NWO;
+    const int wm = wo / (NWO / 2), wn = wo % (NWO / 2);
     const TileId t = tile_of(P, BM, BN);
     const int total = P.cls_th[t.cls].n * P.cls_tw[t.cls].n * (P.c / kTileK);
     Copy cp;
@@ -283,7 +293,8 @@ void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ 
         const u32x4* la = lds + (it % NSTAGE) * STAGE_CHUNKS;
         const u32x4* lb = la + BM * kTileChunks;
 #pragma unroll
-        for (int kk = 0; kk < kTileK / 32; ++kk) {
+        for (int k2 = 0; k2 < kTileK / 32 / KS; ++k2) {
+            const int kk = KS == 2 ? kh : k2;
             const int ch = kk * 4 + (lane >> 4);
             bf16x8 fa[FN], fb[FM];
 #pragma unroll
@@ -304,6 +315,23 @@ void conv_fused_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ 
         cp.advance(P);
     }
     wait_vmcnt<0>();   // no copy into LDS may still be in flight when the workgroup ends
+    if constexpr (KS == 2) {
+        // the second k half hands its partial sums to the first through LDS
+        __syncthreads();   // every wave is done with the copy ring
+        f32x4* red = reinterpret_cast<f32x4*>(lds) + wo * FN * FM * 64 + lane;
+        if (kh == 1) {
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int j = 0; j < FM; ++j) red[(i * FM + j) * 64] = acc[i][j];
+        }
+        __syncthreads();
+        if (kh == 1) return;
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+            for (int j = 0; j < FM; ++j) acc[i][j] += red[(i * FM + j) * 64];
+    }
     store_tile<FM, FN, WM, WN, OT>(P, t, wm, wn, acc, out, epi);
 }
 
@@ -639,12 +667,12 @@ int64_t plan_tiles(FusedPlan& P, int bm, int bn) {
     return t;
 }
 
-template <int BM, int BN, int NS, typename OT, int NW, bool BUF = true>
+template <int BM, int BN, int NS, typename OT, int NW, bool BUF = true, int KS = 1>
 hipError_t go(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
               hipStream_t st) {
     const int64_t tiles = plan_tiles(P, BM, BN);
     if (tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL((conv_fused_kernel<BM, BN, NS, OT, NW, BUF>), dim3((unsigned)tiles),
+    hipLaunchKernelGGL((conv_fused_kernel<BM, BN, NS, OT, NW, BUF, KS>), dim3((unsigned)tiles),
                        dim3(64 * NW), 0, st, (const bf16_t*)x, (const bf16_t*)wt, (OT*)out, P,
                        epi);
     return hipGetLastError();
@@ -685,13 +713,15 @@ hipError_t go_window(FusedPlan& P, const void* x, const void* wt, void* out, con
 // Tile shapes: 0 = 192x128 with 8 waves (one workgroup per CU), 1 = 128x128 with 8 waves
 // (two per CU), 2 = 64x128 with 4 waves, 3 = 64x64 with 8 waves and a 4-stage copy ring;
 // 4-8 = the software-pipelined four-wave form with 192x128, 128x128, 64x64, 128x64 and
-// 256x128 tiles; 9 = the row-window kernel (192x128).  The first of 0, 1, 2 with at least
-// ~one tile per CU is taken, else 6 (the small convolutions: measured fastest of all on
-// the ResNet and DCGAN layers).  The row-window kernel copies 35% fewer bytes on the
-// CSRNet layer in the residue form but measured no faster than 0 there (its copies
-// overlap less with the MFMA work), so it is selected only on request.
-// OLLIE_FUSED_CONFIG overrides the choice (tuning sweeps, tests); 9 falls back to the
-// automatic choice where the row-window form does not apply.
+// 256x128 tiles; 9 = the row-window kernel (192x128); 10-12 = the eight-wave kernel with
+// the k-tile split between the two halves of the waves, 192x128, 128x128 and 64x64
+// (4-stage ring).  Automatic choice: 10 when there is ~one 192x128 tile per CU, else 1
+// or 2 at that count, else 12 (measured fastest on the CSRNet, ResNet and DCGAN layers:
+// 65-68 vs 68-69 us for 0, 12.2 vs 13.8 us and 11.3 vs 12.9 us for 6).  The row-window
+// kernel copies 35% fewer bytes on the CSRNet layer in the residue form but measured no
+// faster than 0 there (its copies overlap less with the MFMA work), so it is selected
+// only on request.  OLLIE_FUSED_CONFIG overrides the choice (tuning sweeps, tests); 9
+// falls back to the automatic choice where the row-window form does not apply.
 template <typename OT>
 hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
                     hipStream_t st) {
@@ -702,12 +732,12 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
     if (P.x_bytes == 0 || P.w_bytes == 0) return go<128, 128, 2, OT, 8, false>(P, x, wt, out, epi, st);
     int cfg = forced;
     if (cfg == 9 && !window_ok(P)) cfg = -1;
-    if (cfg < 0 || cfg > 9) {
+    if (cfg < 0 || cfg > 12) {
         FusedPlan tmp = P;
-        if (plan_tiles(tmp, 192, 128) >= 240) cfg = 0;
+        if (plan_tiles(tmp, 192, 128) >= 240) cfg = 10;
         else if (plan_tiles(tmp, 128, 128) >= 240) cfg = 1;
         else if (plan_tiles(tmp, 64, 128) >= 240) cfg = 2;
-        else cfg = 6;
+        else cfg = 12;
     }
     switch (cfg) {
     case 0: return go<192, 128, 2, OT, 8>(P, x, wt, out, epi, st);
@@ -720,6 +750,9 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
     case 7: return go_pipe<128, 64, 4, OT>(P, x, wt, out, epi, st);
     case 8: return go_pipe<256, 128, 3, OT>(P, x, wt, out, epi, st);
     case 9: return go_window<OT>(P, x, wt, out, epi, st);
+    case 10: return go<192, 128, 2, OT, 8, true, 2>(P, x, wt, out, epi, st);
+    case 11: return go<128, 128, 2, OT, 8, true, 2>(P, x, wt, out, epi, st);
+    case 12: return go<64, 64, 4, OT, 8, true, 2>(P, x, wt, out, epi, st);
     // the small shapes run right after other kernels have evicted their operands: a
     // 4-deep copy ring hides the longer cold loads (measured in the benchmark step)
     default: return go_pipe<64, 64, 4, OT>(P, x, wt, out, epi, st);

@@ -312,6 +312,22 @@ def test_band_small(ci, mask, staged):
     check_band(q, k, v, w, dil, 0.125, mask, staged)
 
 
+# Every wave shape of the fused band kernel (OLLIE_BAND_CONFIG 0-2, read per call): 32
+# or 64 queries per wave, four or two waves per workgroup, on the small cases and a
+# sequence long enough for several workgroups per residue subsequence.
+@pytest.mark.parametrize("ci", range(len(BAND_SMALL) + 1))
+@pytest.mark.parametrize("mask", [False, True])
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_band_every_wave_shape(cfg, mask, ci, monkeypatch):
+    b, l, w, dil = BAND_SMALL[ci] if ci < len(BAND_SMALL) else (2, 1100, 96, 2)
+    say("band wave shape", cfg, (b, l, w, dil), "mask", mask)
+    monkeypatch.setenv("OLLIE_BAND_CONFIG", str(cfg))
+    q = synth.random_tensor((b, l, 64), 14000 + ci, "bf16", dist="normal")
+    k = synth.random_tensor((b, l, 64), 14100 + ci, "bf16", dist="normal")
+    v = synth.random_tensor((b, l, 64), 14200 + ci, "bf16", dist="normal")
+    check_band(q, k, v, w, dil, 0.125, mask, False)
+
+
 @pytest.mark.parametrize("mask", [False, True])
 def test_band_scores_exact_on_integers(mask):
     """Staged G2BMM scores are exact for integer Q, K; softmax rows sum to one."""
@@ -448,7 +464,7 @@ def test_small_shapes_fused(ci, integer):
         assert err(to_np(out), ref) <= TOL_BF16
 
 
-# Every tile shape of the fused expression (OLLIE_FUSED_CONFIG 0-9, read per call), on
+# Every tile shape of the fused expression (OLLIE_FUSED_CONFIG 0-12, read per call), on
 # shapes that exercise the row-window kernel (config 9: stride-1 forms whose class width
 # is a multiple of 16 dividing 192 -- ragged channel tiles, tiles straddling images,
 # kernel widths 1-3) and on shapes where config 9 falls back to the automatic choice.
@@ -464,7 +480,7 @@ TILE_CASES = [
 
 
 @pytest.mark.parametrize("ci", range(len(TILE_CASES)))
-@pytest.mark.parametrize("cfg", range(10))
+@pytest.mark.parametrize("cfg", range(13))
 def test_every_tile_shape_integer_exact(cfg, ci, monkeypatch):
     kind, n, c, h, w, k, r, s, st, pd, dl, op, res = TILE_CASES[ci]
     say("tile shape", cfg, TILE_CASES[ci])
