@@ -313,13 +313,15 @@ def test_band_small(ci, mask, staged):
 
 
 # Every wave shape of the fused band kernel (OLLIE_BAND_CONFIG 0-2, read per call): 32
-# or 64 queries per wave, four or two waves per workgroup, on the small cases and a
-# sequence long enough for several workgroups per residue subsequence.
-@pytest.mark.parametrize("ci", range(len(BAND_SMALL) + 1))
+# or 64 queries per wave, four or two waves per workgroup, on the small cases and
+# sequences long enough for several workgroups per residue subsequence (in the last,
+# the second tile of every odd residue lies past its subsequence).
+@pytest.mark.parametrize("ci", range(len(BAND_SMALL) + 4))
 @pytest.mark.parametrize("mask", [False, True])
 @pytest.mark.parametrize("cfg", [0, 1, 2])
 def test_band_every_wave_shape(cfg, mask, ci, monkeypatch):
-    b, l, w, dil = BAND_SMALL[ci] if ci < len(BAND_SMALL) else (2, 1100, 96, 2)
+    extra = [(2, 1100, 96, 2), (48, 2000, 64, 3), (64, 2600, 40, 1), (300, 257, 16, 2)]
+    b, l, w, dil = BAND_SMALL[ci] if ci < len(BAND_SMALL) else extra[ci - len(BAND_SMALL)]
     say("band wave shape", cfg, (b, l, w, dil), "mask", mask)
     monkeypatch.setenv("OLLIE_BAND_CONFIG", str(cfg))
     q = synth.random_tensor((b, l, 64), 14000 + ci, "bf16", dist="normal")
