@@ -104,6 +104,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--stage", default=None, help="launch only this stage kernel")
+    ap.add_argument("--streams", type=int, default=1, choices=[1, 2, 4],
+                    help="streams the step's independent operators are spread over: 1 = "
+                         "all in order on one stream, 2 = the band beside the three "
+                         "convolutions, 4 = one stream per operator")
     ap.add_argument("--dilated-path", default=None, choices=["staged", "fused", "residues"],
                     help="derived-program variant of the dilated workload (default: PATHS)")
     args = ap.parse_args()
@@ -161,10 +165,37 @@ def main():
         run_stage(args, conv_ops, bwl, q, k, v, o, stream)
         return
 
+    def conv_call(op):
+        op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=op["fused"]))
+
+    # the four operators are independent: with --streams > 1 they are forked from the
+    # current stream onto side streams (default priority) and joined back each step
+    groups = {1: [conv_ops + ["band"]], 2: [conv_ops, ["band"]],
+              4: [[op] for op in conv_ops] + [["band"]]}[args.streams]
+    side = [torch.cuda.Stream(dev) for _ in groups[1:]]
+
+    def run_group(group):
+        for op in group:
+            band_call() if op == "band" else conv_call(op)
+
     def step():
-        for op in conv_ops:
-            op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=op["fused"]))
-        band_call()
+        if not side:
+            run_group(groups[0])
+            return
+        main = torch.cuda.current_stream(dev)
+        fork = torch.cuda.Event()
+        fork.record(main)
+        joins = []
+        for s_, group in zip(side, groups[1:]):
+            s_.wait_event(fork)
+            with torch.cuda.stream(s_):
+                run_group(group)
+                ev = torch.cuda.Event()
+                ev.record(s_)
+                joins.append(ev)
+        run_group(groups[0])
+        for ev in joins:
+            main.wait_event(ev)
 
     for _ in range(args.warmup):
         step()
@@ -287,7 +318,9 @@ def main():
         "config": {"workload": "derived conv3x3 (N16 C256 14x14) + convT4x4s2 (N16 512->256 "
                                "8x8) + dilated conv3x3 d2 (C512 96x128) + band (B96 L4096 d64 "
                                "w256 dil2), bf16 in, fp32 accumulate/out",
-                   "parallelism": "single GPU", "launch": "stream",
+                   "parallelism": "single GPU",
+                   "launch": "stream" if args.streams == 1 else
+                             f"{args.streams} streams (independent operators side by side)",
                    "paths": {op["wl"].name: op["path"] for op in conv_ops}},
         "per_config": per_cfg,
         "roofline": roofline,
