@@ -11,8 +11,9 @@ both variants are timed and reported.
 
 `value` is the step's algorithmic TFLOP/s (all GEMM-stage and band contractions over
 the step time).  Per workload it also reports the GEMM stage in TFLOP/s and % of the
-bf16 MFMA peak, the eOperator stage in GB/s and % of the HBM peak, and the fused
-kernel in TFLOP/s.  Each kernel is timed with HIP events around a HIP graph of
+bf16 MFMA peak (and, since its fp32 Y makes it HBM-bound on these shapes, its HBM
+GB/s and % of the roofline that binds it), the eOperator stage in GB/s and % of the
+HBM peak, and the fused kernel in TFLOP/s.  Each kernel is timed with HIP events around a HIP graph of
 back-to-back launches of that kernel (so host launch gaps do not count) on the stream
 it runs on.  `roofline` covers the kernel that takes the largest share of a step.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workloads.
@@ -268,17 +269,27 @@ def main():
         g_tf = op["flops"] / (g_ms * 1e-3) / 1e12
         e_gb = op["eop_bytes"] / (e_ms * 1e-3) / 1e9
         f_tf = op["flops"] / (f_ms * 1e-3) / 1e12
+        # the GEMM stage's HBM bytes: Y written once, A and B read once
+        g_bytes = op["m"] * op["nc"] * 4 + (op["m"] + op["nc"]) * op["wl"].c * 2
+        g_gb = g_bytes / (g_ms * 1e-3) / 1e9
+        t_mfma = op["flops"] / (PEAK_BF16_TFLOPS * 1e12)
+        t_hbm = g_bytes / (PEAK_HBM_GBS * 1e9)
+        g_bound = "hbm" if t_hbm > t_mfma else "mfma"
         name = op["wl"].name
         per_cfg[name] = {
             "path": op["path"],
             "op_ms": round(k_ms if op["fused"] else g_ms + e_ms, 5),
             "gemm_ms": round(g_ms, 5), "gemm_tflops": round(g_tf, 2),
             "gemm_pct_mfma_peak": round(100 * g_tf / PEAK_BF16_TFLOPS, 2),
+            "gemm_hbm_gbs": round(g_gb, 1), "gemm_pct_hbm_peak": round(100 * g_gb / PEAK_HBM_GBS, 2),
+            "gemm_bound": g_bound,
+            "gemm_pct_roofline": round(100 * max(t_mfma, t_hbm) / (g_ms * 1e-3), 2),
             "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
             "eop_pct_hbm_peak": round(100 * e_gb / PEAK_HBM_GBS, 2),
             "fused_ms": round(f_ms, 5), "fused_tflops": round(f_tf, 2),
             "fused_pct_mfma_peak": round(100 * f_tf / PEAK_BF16_TFLOPS, 2),
-            "gemm_gflop": round(op["flops"] / 1e9, 4), "eop_mbytes": round(op["eop_bytes"] / 1e6, 3),
+            "gemm_gflop": round(op["flops"] / 1e9, 4), "gemm_mbytes": round(g_bytes / 1e6, 3),
+            "eop_mbytes": round(op["eop_bytes"] / 1e6, 3),
         }
         if r_ms is not None:
             per_cfg[name]["fused_residue_form_ms"] = round(r_ms, 5)
@@ -286,8 +297,12 @@ def main():
             kernels.append((f"conv_fused[{name}]", k_ms, "mfma", k_tf, PEAK_BF16_TFLOPS,
                             "TFLOP/s", op["flops"]))
         else:
-            kernels.append((f"gemm_nt[{name}]", g_ms, "mfma", g_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
-                            op["flops"]))
+            if g_bound == "hbm":
+                kernels.append((f"gemm_nt[{name}]", g_ms, "hbm", g_gb, PEAK_HBM_GBS, "GB/s",
+                                g_bytes))
+            else:
+                kernels.append((f"gemm_nt[{name}]", g_ms, "mfma", g_tf, PEAK_BF16_TFLOPS,
+                                "TFLOP/s", op["flops"]))
             kernels.append((f"eop_gather[{name}]", e_ms, "hbm", e_gb, PEAK_HBM_GBS, "GB/s",
                             op["eop_bytes"]))
     b_ms = time_kernel(band_call, reps)

@@ -5,21 +5,26 @@
 // CDNA matrix cores: every lane feeds one row and 8 consecutive k of each operand.
 //
 // bf16 main path (k % 64 == 0): v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
-//   * 64-deep k-tiles of both operands are copied global -> LDS by
-//     global_load_lds_dwordx4 (no register staging).  One such instruction writes
-//     64 lanes x 16 bytes contiguously at the wave-uniform LDS base, so the 16-byte
-//     chunk XOR swizzle (conflict-free ds_read_b128 fragments) is applied on the
-//     source side: the lane that fills LDS chunk slot p of row r fetches logical
-//     chunk p ^ (r & 7).
+//   * 64-deep k-tiles of both operands are copied global -> LDS with no register
+//     staging: raw buffer loads into LDS with 32-bit byte offsets (operands under
+//     2 GiB), else global_load_lds_dwordx4 with 64-bit addresses.  One such
+//     instruction writes 64 lanes x 16 bytes contiguously at the wave-uniform LDS
+//     base, so the 16-byte chunk XOR swizzle (conflict-free ds_read_b128 fragments)
+//     is applied on the source side: the lane that fills LDS chunk slot p of row r
+//     fetches logical chunk p ^ (r & 7).
 //   * NSTAGE LDS buffers form a ring; loads for k-tile kt + NSTAGE - 1 are in flight
 //     while k-tile kt is multiplied, with explicit vmcnt waits.
 //   * Rows past m or n are clamped to the last valid row (their products only reach
 //     rows/columns of Y that are never stored).
+//   * The epilogue stages the finished tile in LDS (the operand ring is free by then)
+//     and writes it row by row: one store instruction covers whole 512-byte rows of
+//     an fp32 tile instead of 64-byte pieces of sixteen rows.  With k as short as it
+//     is here (256-512), Y's write is most of the kernel's HBM traffic.
 // bf16 fallback (any k % 8 == 0): register-staged double-buffered 128x128 tiles.
 // fp32 path: v_mfma_f32_16x16x4_f32 (small problems; any k).
 //
 // The MFMA is issued as D = Wt-tile x X-tile^T so that each lane ends up holding four
-// consecutive output columns n of one row m: the epilogue writes 16-byte vectors.
+// consecutive output columns n of one row m.
 #include <stdlib.h>
 
 #include "common.h"
@@ -80,60 +85,111 @@ __device__ __forceinline__ void store_tile(YT* __restrict__ Y, const f32x4 (&acc
 }
 
 // ------------------------------------------------------------------ main bf16 path
-template <int BM, int BN, int BK, int NSTAGE, typename YT>
-__global__ __launch_bounds__(256, (NSTAGE * (BM + BN) * BK * 2 <= 80 * 1024) ? 2 : 1)
+// Epilogue through LDS: the tile's rows (BN values, 16-byte chunks XOR-swizzled by
+// row & 15, so that both the fragment writes and the row reads are conflict free)
+// are staged in `lds` in passes of RP rows and stored row-contiguously.
+template <int BM, int BN, int NT, int LDS_CHUNKS, int WM, int WN, int FM, int FN, typename YT>
+__device__ __forceinline__ void store_tile_rows(YT* __restrict__ Y, const f32x4 (&acc)[FN][FM],
+                                                u32x4* lds, int64_t M, int64_t N, int64_t m0,
+                                                int64_t n0, int wm, int wn) {
+    constexpr int CH = BN / 4;                       // 16-byte fp32 chunks per tile row
+    static_assert(CH >= 16, "swizzle needs at least 16 chunks per row");
+    constexpr int FIT = LDS_CHUNKS / CH;             // rows that fit in LDS at once
+    constexpr int RP = FIT >= BM ? BM : FIT >= BM / 2 ? BM / 2 : BM / 4;
+    constexpr int PASSES = BM / RP;
+    static_assert(RP % 16 == 0 && RP <= FIT && (RP * CH) % NT == 0, "epilogue passes");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const bool vec_ok = (N & 3) == 0;
+    f32x4* t = reinterpret_cast<f32x4*>(lds);
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+        __syncthreads();    // the previous readers of these LDS bytes are done
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+            if ((wm * WM + j * 16) / RP != p) continue;
+            const int r = (wm * WM + j * 16) % RP + (lane & 15);
+#pragma unroll
+            for (int i = 0; i < FN; ++i) {
+                const int c = (wn * WN + i * 16) / 4 + (lane >> 4);
+                t[r * CH + (c ^ (r & 15))] = acc[i][j];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int it = 0; it < RP * CH / NT; ++it) {
+            const int e = it * NT + tid;
+            const int r = e / CH, c = e % CH;
+            const f32x4 v = t[r * CH + (c ^ (r & 15))];
+            const int64_t m = m0 + p * RP + r, n = n0 + 4 * c;
+            if (m >= M) continue;
+            YT* dst = Y + m * N + n;
+            if (vec_ok && n + 3 < N) {
+                Out<YT>::put4(dst, v);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (n + q < N) Out<YT>::put(dst + q, v[q]);
+            }
+        }
+    }
+}
+
+// BUF: operands addressed by 32-bit byte offsets through buffer loads (each operand
+// under 2 GiB); otherwise 64-bit global addresses.
+template <int BM, int BN, int NSTAGE, int WAVES_M, int WAVES_N, int MINB, bool BUF, typename YT>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, MINB)
 void gemm_nt_bf16_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
                              YT* __restrict__ Y, int64_t M, int64_t N, int64_t K, int tiles_m,
                              int tiles_n) {
-    constexpr int WM = BM / 2, WN = BN / 2;        // wave sub-tile (2 x 2 waves)
-    constexpr int FM = WM / 16, FN = WN / 16;      // 16x16 MFMA blocks per wave
-    constexpr int CPR = BK / 8;                    // 16-byte chunks per tile row
-    constexpr int RPI = 64 / CPR;                  // tile rows per wave-wide DMA instruction
-    constexpr int ROWS = BM + BN;                  // tile rows per stage (A rows, then B rows)
-    constexpr int STAGE_CHUNKS = ROWS * CPR;
-    constexpr int LOADS = STAGE_CHUNKS / 256;      // DMA instructions per wave per stage
-    static_assert(STAGE_CHUNKS % 256 == 0, "stage must be a whole number of wave loads");
+    constexpr int NW = WAVES_M * WAVES_N, NT = 64 * NW;
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;   // wave sub-tile
+    constexpr int FM = WM / 16, FN = WN / 16;             // 16x16 MFMA blocks per wave
+    constexpr int RPI = 64 / kChunks;                     // tile rows per wave-wide copy
+    constexpr int STAGE_CHUNKS = (BM + BN) * kChunks;     // A rows, then B rows
+    constexpr int LOADS = STAGE_CHUNKS / NT;              // copies per wave per stage
+    constexpr int A_LOADS = BM * kChunks / NT;            // the first A_LOADS copy A rows
+    static_assert(STAGE_CHUNKS % NT == 0 && (BM * kChunks) % NT == 0, "whole wave copies");
     __shared__ u32x4 lds[NSTAGE * STAGE_CHUNKS];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     int tm, tn;
     tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
 
-    // Per-lane source rows for this wave's DMA instructions.  Instruction i of wave w
-    // fills LDS chunk slots [(i*4 + w)*64, +64): rows (i*4+w)*RPI + lane/CPR, slot lane%CPR.
-    const bf16_t* src[LOADS];
+    // Copy i of wave w fills LDS chunk slots [(i*NW + w)*64, +64): rows
+    // (i*NW + w)*RPI + lane/8, slot lane%8, which holds logical chunk slot ^ (row & 7).
+    int64_t off[LOADS];                                   // element offset of each lane's chunk
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
-        const int row = (i * 4 + wave) * RPI + lane / CPR;
-        const int slot = lane % CPR;
-        // the lane filling slot `slot` of `row` fetches the chunk the swizzle puts there
-        int ch = 0;
-#pragma unroll
-        for (int c = 0; c < CPR; ++c)
-            if (tile_swz_k<BK>(row, c) - row * CPR == slot) ch = c;
-        const bf16_t* p;
-        if (row < BM) {
-            int64_t gm = m0 + row;
-            gm = gm < M ? gm : M - 1;
-            p = A + gm * K + ch * 8;
+        const int row = (i * NW + wave) * RPI + lane / kChunks;
+        const int ch = (lane % kChunks) ^ (row & 7);
+        int64_t g;
+        if (i < A_LOADS) {
+            g = m0 + row;
+            g = g < M ? g : M - 1;
         } else {
-            int64_t gn = n0 + (row - BM);
-            gn = gn < N ? gn : N - 1;
-            p = B + gn * K + ch * 8;
+            g = n0 + (row - BM);
+            g = g < N ? g : N - 1;
         }
-        src[i] = p;
+        off[i] = g * K + ch * 8;
     }
+    const int a_bytes = BUF ? (int)(M * K * 2) : 0, b_bytes = BUF ? (int)(N * K * 2) : 0;
     auto issue = [&](int kt, int buf) {
-        const int64_t koff = (int64_t)kt * BK;
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i)
-            __builtin_amdgcn_global_load_lds(
-                (const void*)(src[i] + koff),
-                (lds_void*)(lds + buf * STAGE_CHUNKS + (i * 4 + wave) * 64), 16, 0, 0);
+        for (int i = 0; i < LOADS; ++i) {
+            const bool is_a = i < A_LOADS;
+            lds_void* dst = (lds_void*)(lds + buf * STAGE_CHUNKS + (i * NW + wave) * 64);
+            if constexpr (BUF) {
+                buffer_copy16(is_a ? (const void*)A : (const void*)B, is_a ? a_bytes : b_bytes,
+                              (uint32_t)(off[i] * 2), kt * kBK * 2, dst);
+            } else {
+                const bf16_t* src = (is_a ? A : B) + off[i] + (int64_t)kt * kBK;
+                __builtin_amdgcn_global_load_lds((const void*)src, dst, 16, 0, 0);
+            }
+        }
     };
 
     f32x4 acc[FN][FM];
@@ -142,7 +198,7 @@ void gemm_nt_bf16_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restr
 #pragma unroll
         for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-    const int ktiles = (int)(K / BK);
+    const int ktiles = (int)(K / kBK);
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s)
         if (s < ktiles) issue(s, s);
@@ -154,145 +210,6 @@ void gemm_nt_bf16_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restr
         __builtin_amdgcn_s_barrier();   // every wave's part of tile kt is in LDS; tile kt-1 is consumed
         if (kt + NSTAGE - 1 < ktiles) issue(kt + NSTAGE - 1, (kt + NSTAGE - 1) % NSTAGE);
         const u32x4* la = lds + (kt % NSTAGE) * STAGE_CHUNKS;
-        const u32x4* lb = la + BM * CPR;
-#pragma unroll
-        for (int kk = 0; kk < BK / 32; ++kk) {
-            const int ch = kk * 4 + (lane >> 4);
-            bf16x8 fa[FN], fb[FM];
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-                fa[i] = __builtin_bit_cast(
-                    bf16x8, lb[tile_swz_k<BK>(wn * WN + i * 16 + (lane & 15), ch)]);
-#pragma unroll
-            for (int j = 0; j < FM; ++j)
-                fb[j] = __builtin_bit_cast(
-                    bf16x8, la[tile_swz_k<BK>(wm * WM + j * 16 + (lane & 15), ch)]);
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-#pragma unroll
-                for (int j = 0; j < FM; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j],
-                                                                        0, 0, 0);
-        }
-    }
-    store_tile<FM, FN, YT>(Y, acc, M, N, m0 + wm * WM, n0 + wn * WN);
-}
-
-// --------------------------------------------------------- persistent bf16 path
-// One workgroup per CU walks a strided list of tiles.  The LDS ring runs across tile
-// boundaries: the first k-tiles of the next tile are already in flight while the
-// current tile finishes, and its Y stores drain under the next tile's loads and MFMAs.
-// The vmcnt bookkeeping assumes vector-memory operations retire in issue order: at
-// iteration `it` the wait allows exactly the loads issued for later k-tiles plus the
-// stores of an epilogue issued after k-tile `it`'s loads.  Interior tiles store with a
-// fixed instruction count; a tile with ragged rows or columns waits for everything.
-template <int BM, int BN, int NSTAGE, int WAVES_M, int WAVES_N, typename YT>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_nt_bf16_persistent_kernel(
-    const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, YT* __restrict__ Y,
-    int64_t M, int64_t N, int64_t K, int tiles_m, int tiles_n) {
-    constexpr int NW = WAVES_M * WAVES_N;
-    constexpr int NT = 64 * NW;
-    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-    constexpr int FM = WM / 16, FN = WN / 16;
-    constexpr int ROWS = BM + BN;
-    constexpr int STAGE_CHUNKS = ROWS * kChunks;
-    constexpr int LOADS = STAGE_CHUNKS / NT;          // DMA instructions per wave per stage
-    constexpr int A_LOADS = BM * kChunks / NT;        // the first A_LOADS of them fetch A rows
-    constexpr int STORES = FM * FN;                   // store instructions of an interior epilogue
-    static_assert(STAGE_CHUNKS % NT == 0 && (BM * kChunks) % NT == 0, "whole wave loads");
-    // waits allow at most 63 outstanding operations; a larger count is clamped, which
-    // only makes the wait stricter (operations retire in order)
-    constexpr int W_LS = LOADS * (NSTAGE - 2) + STORES < 63 ? LOADS * (NSTAGE - 2) + STORES : 63;
-    constexpr int W_L = LOADS * (NSTAGE - 2) < 63 ? LOADS * (NSTAGE - 2) : 63;
-    constexpr int W_S = STORES < 63 ? STORES : 63;
-    __shared__ u32x4 lds[NSTAGE * STAGE_CHUNKS];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-    const int ntiles = tiles_m * tiles_n;
-    const int G = gridDim.x;
-    const int w = blockIdx.x;
-    // XCD-compact assignment: at round i, the G/8 workgroups of one XCD take a
-    // contiguous run of the grouped tile order.
-    const int slot = (G & 7) == 0 ? (w & 7) * (G >> 3) + (w >> 3) : w;
-    const int my_tiles = slot < ntiles ? (ntiles - 1 - slot) / G + 1 : 0;
-    const int ktiles = (int)(K / kBK);
-    const int total = my_tiles * ktiles;
-
-    auto coords = [&](int i, int64_t& m0, int64_t& n0) {
-        // grouped order only (the XCD spreading is already in `slot`)
-        const int id = i * G + slot;
-        const int group_m = 8;
-        const int group = id / (group_m * tiles_n);
-        const int first_m = group * group_m;
-        const int gsize = tiles_m - first_m < group_m ? tiles_m - first_m : group_m;
-        const int in_group = id - group * group_m * tiles_n;
-        m0 = (int64_t)(first_m + in_group % gsize) * BM;
-        n0 = (int64_t)(in_group / gsize) * BN;
-    };
-    auto issue = [&](int it) {
-        const int ti = it / ktiles, kt = it - ti * ktiles;
-        int64_t m0, n0;
-        coords(ti, m0, n0);
-        const int buf = it % NSTAGE;
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int seg = i * NW + wave;
-            const int row = seg * 8 + (lane >> 3);
-            const int ch = (lane & 7) ^ (row & 7);
-            const bf16_t* p;
-            if (i < A_LOADS) {
-                int64_t gm = m0 + row;
-                gm = gm < M ? gm : M - 1;
-                p = A + gm * K;
-            } else {
-                int64_t gn = n0 + (row - BM);
-                gn = gn < N ? gn : N - 1;
-                p = B + gn * K;
-            }
-            __builtin_amdgcn_global_load_lds((const void*)(p + (int64_t)kt * kBK + ch * 8),
-                                             (lds_void*)(lds + buf * STAGE_CHUNKS + seg * 64),
-                                             16, 0, 0);
-        }
-    };
-
-    f32x4 acc[FN][FM];
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-    for (int s = 0; s < NSTAGE - 1; ++s)
-        if (s < total) issue(s);
-
-    int last_epi = -1000;       // iteration whose epilogue was the most recent
-    bool last_epi_edge = false;
-    for (int it = 0; it < total; ++it) {
-        // loads issued after k-tile it's: min(NSTAGE-2, total-1-it) stages; stores after
-        // it: an epilogue at iteration e in [it-NSTAGE+1, it-1]
-        const int later = (total - 1 - it) < (NSTAGE - 2) ? (total - 1 - it) : (NSTAGE - 2);
-        const bool epi = last_epi >= it - NSTAGE + 1;
-        if (epi && last_epi_edge) {
-            wait_vmcnt<0>();
-        } else if constexpr (NSTAGE == 3) {
-            if (later == 1) {
-                if (epi) wait_vmcnt<W_LS>();
-                else wait_vmcnt<W_L>();
-            } else {
-                if (epi) wait_vmcnt<W_S>();
-                else wait_vmcnt<0>();
-            }
-        } else {
-            static_assert(NSTAGE == 2, "two or three stages");
-            if (epi) wait_vmcnt<W_S>();
-            else wait_vmcnt<0>();
-        }
-        __builtin_amdgcn_s_barrier();
-        if (it + NSTAGE - 1 < total) issue(it + NSTAGE - 1);
-        const u32x4* la = lds + (it % NSTAGE) * STAGE_CHUNKS;
         const u32x4* lb = la + BM * kChunks;
 #pragma unroll
         for (int kk = 0; kk < kBK / 32; ++kk) {
@@ -311,30 +228,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_nt_bf16_persis
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j],
                                                                         0, 0, 0);
         }
-        if ((it + 1) % ktiles == 0) {
-            int64_t m0, n0;
-            coords(it / ktiles, m0, n0);
-            const bool interior = m0 + BM <= M && n0 + BN <= N && (N & 3) == 0;
-            const int64_t mb = m0 + wm * WM, nb = n0 + wn * WN;
-            if (interior) {
-#pragma unroll
-                for (int j = 0; j < FM; ++j) {
-                    const int64_t m = mb + j * 16 + (lane & 15);
-#pragma unroll
-                    for (int i = 0; i < FN; ++i)
-                        Out<YT>::put4(Y + m * N + nb + i * 16 + 4 * (lane >> 4), acc[i][j]);
-                }
-            } else {
-                store_tile<FM, FN, YT>(Y, acc, M, N, mb, nb);
-            }
-            last_epi = it;
-            last_epi_edge = !interior;
-#pragma unroll
-            for (int i = 0; i < FN; ++i)
-#pragma unroll
-                for (int j = 0; j < FM; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        }
     }
+    store_tile_rows<BM, BN, NT, NSTAGE * STAGE_CHUNKS, WM, WN, FM, FN, YT>(Y, acc, lds, M, N, m0,
+                                                                           n0, wm, wn);
 }
 
 // -------------------------------------------------------- register-staged bf16 fallback
@@ -482,74 +378,45 @@ __global__ __launch_bounds__(256) void gemm_nt_f32_kernel(
     store_tile<2, 2, YT>(Y, acc, M, N, m0 + wm * 32, n0 + wn * 32);
 }
 
-template <int BM, int BN, int BK, int NSTAGE, typename YT>
+template <int BM, int BN, int NSTAGE, int WAVES_M, int WAVES_N, int MINB, bool BUF, typename YT>
 hipError_t go_dma(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
                   hipStream_t stream) {
     int tiles_m = (int)((m + BM - 1) / BM), tiles_n = (int)((n + BN - 1) / BN);
-    hipLaunchKernelGGL((gemm_nt_bf16_dma_kernel<BM, BN, BK, NSTAGE, YT>), dim3(tiles_m * tiles_n),
-                       dim3(256), 0, stream, (const bf16_t*)a, (const bf16_t*)b, (YT*)y, m, n, k,
-                       tiles_m, tiles_n);
+    hipLaunchKernelGGL((gemm_nt_bf16_dma_kernel<BM, BN, NSTAGE, WAVES_M, WAVES_N, MINB, BUF, YT>),
+                       dim3(tiles_m * tiles_n), dim3(64 * WAVES_M * WAVES_N), 0, stream,
+                       (const bf16_t*)a, (const bf16_t*)b, (YT*)y, m, n, k, tiles_m, tiles_n);
     return hipGetLastError();
 }
 
-int num_cus() {
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-            n = 256;
-        cached[dev] = n;
-    }
-    return cached[dev];
-}
-
-template <int BM, int BN, int NSTAGE, int WAVES_M, int WAVES_N, typename YT>
-hipError_t go_persistent(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
-                         hipStream_t stream) {
-    const int tiles_m = (int)((m + BM - 1) / BM), tiles_n = (int)((n + BN - 1) / BN);
-    const int ntiles = tiles_m * tiles_n;
-    const int cus = num_cus();
-    const int grid = ntiles < cus ? ntiles : cus;
-    hipLaunchKernelGGL((gemm_nt_bf16_persistent_kernel<BM, BN, NSTAGE, WAVES_M, WAVES_N, YT>),
-                       dim3(grid), dim3(64 * WAVES_M * WAVES_N), 0, stream, (const bf16_t*)a,
-                       (const bf16_t*)b, (YT*)y, m, n, k, tiles_m, tiles_n);
-    return hipGetLastError();
-}
-
-// Tile configuration of the DMA kernels: 0 = 256x128, 3 stages (one workgroup per CU);
-// 1 = 128x128, 3 stages (one per CU); 2 = 128x128, 2 stages (two per CU);
-// 3 = persistent 256x256, 2 stages, 8 waves; 4 = persistent 256x128, 3 stages, 4 waves;
-// 5 = 128x256 and 6 = 256x128 with 32-deep k-tiles, 3 stages (two workgroups per CU);
-// 7 = 128x128, 32-deep k-tiles, 4 stages.
-// OLLIE_GEMM_CONFIG (0..7) overrides the shape-based choice, for tuning sweeps.
+// Tile configurations of the DMA kernel (BM x BN, waves, ring stages, workgroups per CU
+// that fit in LDS):
+//   0 = 128x128, 4 waves, 2 stages, two per CU      1 = 128x128, 8 waves, 2 stages, two per CU
+//   2 = 64x128, 4 waves, 2 stages, three per CU     3 = 128x128, 4 waves, 3 stages, one per CU
+//   4 = 256x128, 8 waves, 2 stages, one per CU
+// OLLIE_GEMM_CONFIG (0..4, read per call) overrides the shape-based choice.
+constexpr int kGemmConfigs = 5;
 int pick_config(int64_t m, int64_t n) {
-    static const int forced = [] {
-        const char* e = getenv("OLLIE_GEMM_CONFIG");
-        return e ? atoi(e) : -1;
-    }();
-    if (forced >= 0 && forced <= 7) return forced;
+    const char* e = getenv("OLLIE_GEMM_CONFIG");
+    const int forced = e ? atoi(e) : -1;
+    if (forced >= 0 && forced < kGemmConfigs) return forced;
+    // up to one 128x128 tile per CU: halve the tile height to give every CU work
     const int64_t t128 = ((m + 127) / 128) * ((n + 127) / 128);
-    if (t128 > 256) return 2;           // two workgroups per CU hide each other's latency
-    return 1;
+    return t128 <= 256 ? 2 : 1;
 }
 
 template <typename YT>
 hipError_t go_bf16(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
                    hipStream_t stream) {
     if (k % kBK == 0) {
-        int cfg = pick_config(m, n);
-        if (cfg >= 3 && k / kBK < 2) cfg = 2;    // the cross-tile ring needs >= 2 k-tiles
-        switch (cfg) {
-        case 3: return go_persistent<256, 256, 2, 2, 4, YT>(m, n, k, a, b, y, stream);
-        case 4: return go_persistent<256, 128, 3, 2, 2, YT>(m, n, k, a, b, y, stream);
-        case 0: return go_dma<256, 128, 64, 3, YT>(m, n, k, a, b, y, stream);
-        case 1: return go_dma<128, 128, 64, 3, YT>(m, n, k, a, b, y, stream);
-        case 5: return go_dma<128, 256, 32, 3, YT>(m, n, k, a, b, y, stream);
-        case 6: return go_dma<256, 128, 32, 3, YT>(m, n, k, a, b, y, stream);
-        case 7: return go_dma<128, 128, 32, 4, YT>(m, n, k, a, b, y, stream);
-        default: return go_dma<128, 128, 64, 2, YT>(m, n, k, a, b, y, stream);
+        // buffer offsets are 32-bit: larger operands take the 64-bit address form
+        if (m * k * 2 >= (int64_t(1) << 31) || n * k * 2 >= (int64_t(1) << 31))
+            return go_dma<128, 128, 2, 2, 2, 2, false, YT>(m, n, k, a, b, y, stream);
+        switch (pick_config(m, n)) {
+        case 1: return go_dma<128, 128, 2, 2, 4, 2, true, YT>(m, n, k, a, b, y, stream);
+        case 2: return go_dma<64, 128, 2, 2, 2, 3, true, YT>(m, n, k, a, b, y, stream);
+        case 3: return go_dma<128, 128, 3, 2, 2, 1, true, YT>(m, n, k, a, b, y, stream);
+        case 4: return go_dma<256, 128, 2, 4, 2, 1, true, YT>(m, n, k, a, b, y, stream);
+        default: return go_dma<128, 128, 2, 2, 2, 2, true, YT>(m, n, k, a, b, y, stream);
         }
     }
     int tiles_m = (int)((m + 127) / 128), tiles_n = (int)((n + 127) / 128);

@@ -147,3 +147,12 @@ def random_tensor(shape, seed: int, dtype: str = "f32", integer: bool = False,
     else:
         t = _draw(tuple(shape), dist, 1.0, g)
     return _round(t, dtype)
+
+
+def device_integer_tensor(shape, seed: int, device, dtype=torch.bfloat16) -> torch.Tensor:
+    """A seeded integer-valued tensor (values in {-3..3}) drawn directly on `device`,
+    for operands too large to draw on the CPU and copy over (multi-GiB cases that
+    are checked on sampled outputs)."""
+    g = torch.Generator(device=device).manual_seed(seed)
+    t = torch.randint(-3, 4, tuple(shape), generator=g, device=device, dtype=torch.int8)
+    return t.to(dtype)

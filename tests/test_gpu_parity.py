@@ -182,8 +182,8 @@ def test_small_shapes_bf16(ci, integer):
 # ----------------------------------------------------------------- stage entry points
 
 # k % 64 != 0 takes the register-staged kernel; k % 64 == 0 the DMA kernel, whose tile
-# configuration follows the shape: (4129, 4136) -> 256x128/3 stages, (2100, 2100) ->
-# 128x128/2 stages, the others -> 128x128/3 stages (all with ragged m and n tails).
+# configuration follows the shape: (2100, 2100) and (4129, 4136) -> 128x128 tiles of eight
+# waves, the others -> 64x128 tiles (all with ragged m and n tails).
 @pytest.mark.parametrize("m,n,k", [(1, 1, 8), (129, 257, 72), (300, 130, 200), (64, 64, 64),
                                    (200, 300, 128), (300, 130, 192), (2100, 2100, 64),
                                    (4129, 4136, 128)])
@@ -195,6 +195,49 @@ def test_gemm_stage_bf16_integer_exact(m, n, k):
     torch.cuda.synchronize()
     ref = a.double().numpy() @ b.double().numpy().T
     assert np.array_equal(to_np(y), ref)
+
+
+GEMM_CONFIGS = 5
+
+
+@pytest.mark.parametrize("cfg", range(GEMM_CONFIGS))
+@pytest.mark.parametrize("m,n,k", [(129, 257, 128), (300, 130, 192), (1000, 522, 64),
+                                   (64, 64, 512), (260, 1030, 256)])
+@pytest.mark.parametrize("y_bf16", [False, True])
+def test_gemm_every_tile_config_integer_exact(monkeypatch, cfg, m, n, k, y_bf16):
+    """Every DMA tile configuration on integer inputs: exact fp32 Y, and a bf16 Y equal
+    to the exact sum rounded to nearest even (n = 522 is not a multiple of 4, so the
+    row stores take their element-wise tail)."""
+    monkeypatch.setenv("OLLIE_GEMM_CONFIG", str(cfg))
+    say("gemm cfg", cfg, m, n, k, "bf16 y" if y_bf16 else "fp32 y")
+    a = synth.random_tensor((m, k), 6100 + m, "bf16", integer=True)
+    b = synth.random_tensor((n, k), 7100 + n, "bf16", integer=True)
+    y = ol.gemm_nt(a.to(DEV), b.to(DEV), y_dtype=torch.bfloat16 if y_bf16 else torch.float32)
+    torch.cuda.synchronize()
+    ref = a.double().numpy() @ b.double().numpy().T
+    if y_bf16:
+        assert torch.equal(y.cpu(), torch.from_numpy(ref).to(torch.bfloat16))
+    else:
+        assert np.array_equal(to_np(y), ref)
+
+
+def test_gemm_stage_operand_over_2gib_sampled():
+    """An A operand over 2 GiB takes the 64-bit address form of the DMA kernel; sampled
+    rows (first, last, around the 2 GiB byte boundary and random) are exact."""
+    m, n, k = (1 << 21) + 37, 72, 512
+    say("gemm over 2 GiB", m, n, k)
+    a = synth.device_integer_tensor((m, k), 6200, DEV)
+    b = synth.device_integer_tensor((n, k), 6201, DEV)
+    y = ol.gemm_nt(a, b)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(6202)
+    rows = sorted(set([0, 1, (1 << 21) - 1, 1 << 21, m - 2, m - 1]
+                      + rng.integers(0, m, 250).tolist()))
+    idx = torch.tensor(rows, device=DEV)
+    ref = a[idx].double().cpu().numpy() @ b.double().cpu().numpy().T
+    assert np.array_equal(y[idx].cpu().numpy().astype(np.float64), ref)
+    del a, y
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("m,n,k", [(1, 1, 1), (70, 33, 17), (200, 100, 45)])
