@@ -275,6 +275,46 @@ def test_eop_stage_alone(transposed):
     assert np.array_equal(to_np(out), ref)
 
 
+# (transposed, x shape, r, s, k, stride, pad, dil, out_pad): the unrolled-tap eOperator
+# kernel with 2 and 3 candidates per axis (forward; transposed with tap steps 1, 2 and
+# 3), the loop kernel (5x5 taps; k % 4 != 0; a grid over 2^20 threads).
+EOP_CASES = [
+    (False, (2, 9, 7, 8), 3, 3, 12, (1, 2), (2, 1), (2, 1), (0, 0)),
+    (False, (1, 6, 5, 8), 2, 1, 8, (1, 1), (1, 0), (1, 1), (0, 0)),
+    (False, (1, 8, 8, 8), 5, 5, 8, (1, 1), (2, 2), (1, 1), (0, 0)),
+    (True, (2, 5, 6, 8), 4, 4, 12, (2, 2), (1, 1), (1, 1), (1, 1)),
+    (True, (1, 5, 5, 8), 3, 3, 8, (1, 1), (1, 1), (1, 1), (0, 0)),
+    (True, (1, 5, 6, 8), 3, 3, 8, (2, 2), (1, 2), (2, 2), (1, 1)),
+    (True, (1, 4, 5, 8), 3, 3, 8, (3, 3), (1, 1), (2, 2), (2, 1)),
+    (False, (1, 9, 7, 8), 3, 3, 6, (1, 1), (1, 1), (1, 1), (0, 0)),
+    (False, (1, 130, 128, 8), 3, 3, 256, (1, 1), (1, 1), (1, 1), (0, 0)),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(EOP_CASES)))
+@pytest.mark.parametrize("y_bf16", [False, True])
+def test_eop_kernels_integer_exact(ci, y_bf16):
+    """The eOperator stage alone on an integer scope Y (exact in bf16 too), against the
+    NumPy derived-form eOperator, for every kernel choice."""
+    tr, shape, r, s, k, st, pd, dl, op = EOP_CASES[ci]
+    say("eop kernels", EOP_CASES[ci], "bf16 y" if y_bf16 else "fp32 y")
+    x = synth.random_tensor(shape, 10100 + ci, integer=True)
+    wt = synth.random_tensor((r, s, k, shape[3]), 10200 + ci, integer=True)
+    y = dfm.gemm_stage(x.numpy(), wt.numpy())
+    if tr:
+        ref = dfm.selective_add(y, x.shape, wt.shape, st, pd, dl, op)
+    else:
+        ref = dfm.offset_add(y, x.shape, wt.shape, st, pd, dl)
+    desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), st, pd, dl, op, torch.float32,
+                        torch.float32)
+    yt = torch.as_tensor(y, dtype=torch.float32)
+    if y_bf16:
+        yt = yt.to(torch.bfloat16)
+    out = ol.eop_gather(desc, tr, yt.to(DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out), ref)
+
+
 def test_outputs_stay_in_bounds_and_runs_are_deterministic():
     wl = synth.WORKLOADS[3]
     say("canary + determinism, workload 3")
