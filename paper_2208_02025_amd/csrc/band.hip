@@ -416,13 +416,13 @@ __global__ __launch_bounds__(64 * NW, HQ <= 2 ? 4 : 2) void band_fused_kernel(Ba
     const char* vseq = reinterpret_cast<const char*>(V + seq0);
     const uint32_t row_bytes = (uint32_t)g.dil * kD * 2;
     const char* zero = reinterpret_cast<const char*>(kBandZero);
-    int tt0 = t.q0 - w + dr;                         // key of row dr of block 0
-    uint32_t boff = (uint32_t)tt0 * row_bytes + dch * 16;   // used only when tt0 >= 0
+    const int tt0 = t.q0 - w + dr;                   // key of row dr of block 0
     // buffer form: byte offsets from the start of the residue subsequence; a key before
     // it (negative offset, >= 2^31 as unsigned) or after it lies outside the buffer's
-    // range and reads zeros, so every block takes the same two loads per pass
-    const int nrec = (t.lr - 1) * (int)row_bytes + kD * 2;
-    const int voff0 = tt0 * (int)row_bytes + dch * 16;
+    // range and reads zeros, so every block takes the same two loads per pass.  The
+    // launch takes this form only when every such offset fits in 32 bits.
+    const int nrec = BUF ? (t.lr - 1) * (int)row_bytes + kD * 2 : 0;
+    const int voff0 = BUF ? tt0 * (int)row_bytes + dch * 16 : 0;
     auto dma = [&](int kb) {
         u32x4* slot = lds + (kb % kSlots) * kSlotChunks;
         if constexpr (BUF) {
@@ -434,12 +434,13 @@ __global__ __launch_bounds__(64 * NW, HQ <= 2 ? 4 : 2) void band_fused_kernel(Ba
             }
             return;
         }
+        // 64-bit form: a subsequence may span more than 4 GiB
         const int tt = tt0 + kb * kT;
-        const uint32_t off = boff + (uint32_t)(kb * kT) * row_bytes;
         if (t.q0 - w + kb * kT >= 0 && t.q0 - w + kb * kT + kT <= t.lr) {   // interior block
+            const int64_t off = (int64_t)tt * row_bytes + dch * 16;
 #pragma unroll
             for (int e = 0; e < kPass; ++e) {
-                const uint32_t o2 = off + e * NW * 8 * row_bytes;
+                const int64_t o2 = off + (int64_t)(e * NW * 8) * row_bytes;
                 __builtin_amdgcn_global_load_lds((const void*)(kseq + o2),
                                                  (lds_void*)(slot + (e * NW + wv) * 64), 16, 0,
                                                  0);
@@ -452,7 +453,7 @@ __global__ __launch_bounds__(64 * NW, HQ <= 2 ? 4 : 2) void band_fused_kernel(Ba
             for (int e = 0; e < kPass; ++e) {
                 const int te = tt + NW * 8 * e;
                 const bool ok = te >= 0 && te < t.lr;
-                const uint32_t o2 = (uint32_t)te * row_bytes + dch * 16;
+                const int64_t o2 = (int64_t)te * row_bytes + dch * 16;
                 __builtin_amdgcn_global_load_lds((const void*)(ok ? kseq + o2 : zero),
                                                  (lds_void*)(slot + (e * NW + wv) * 64), 16, 0,
                                                  0);

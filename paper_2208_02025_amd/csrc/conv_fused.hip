@@ -126,7 +126,7 @@ struct TileCopy {
             // an out-of-range row reads zeros: its coordinates are pushed off the image
             hi0[i] = m < t.mc ? P.alpha_h * ii : -(1 << 28);
             wi0[i] = P.alpha_w * jj;
-            rowpix[i] = (nn * H + hi0[i]) * W + wi0[i];
+            rowpix[i] = m < t.mc ? (nn * H + hi0[i]) * W + wi0[i] : 0;   // read only if valid
         }
 #pragma unroll
         for (int i = 0; i < B; ++i) {

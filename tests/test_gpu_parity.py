@@ -197,6 +197,25 @@ def test_gemm_stage_bf16_integer_exact(m, n, k):
     assert np.array_equal(to_np(y), ref)
 
 
+def test_fused_conv_input_over_2gib_sampled():
+    """An input X over 2 GiB takes the fused kernel's 64-bit address form; whole output
+    rows (top, bottom, and on both sides of the row that starts at byte 2^31 of X) are
+    exact against the oracle run on the input rows each output row reads."""
+    n, h, w, c, k = 1, 2049, 1024, 512, 16
+    say("fused conv over 2 GiB", n, h, w, c, k)
+    x = synth.device_integer_tensor((n, h, w, c), 6400, DEV)
+    wt = synth.device_integer_tensor((3, 3, k, c), 6401, DEV)
+    out = ol.derived_conv2d(x, wt, 1, 1, fuse=True)
+    torch.cuda.synchronize()
+    wt_c = wt.float().cpu()
+    for ho in [0, 1000, 2046, 2047, 2048]:
+        lo, hi = max(0, ho - 1), min(h, ho + 2)
+        ref = oracle.conv2d(x[:, lo:hi].float().cpu(), wt_c, 1, 1, 1)[:, ho - lo]
+        assert np.array_equal(out[:, ho].cpu().numpy().astype(np.float64), ref), ho
+    del x, out
+    torch.cuda.empty_cache()
+
+
 GEMM_CONFIGS = 5
 
 
@@ -466,6 +485,36 @@ def test_band_fused_and_staged_agree_at_full_size():
     assert torch.isfinite(o1).all() and torch.isfinite(o2).all()
     d = (o1 - o2).abs().max().item() / o2.abs().max().item()
     assert d <= TOL_BF16
+
+
+@pytest.mark.parametrize("mask", [False, True])
+def test_band_subsequence_over_4gib_sampled(mask):
+    """A residue subsequence whose keys span more than 4 GiB takes the band kernel's
+    64-bit address form.  Sampled query rows (sequence ends, and keys on both sides of
+    the 2^31- and 2^32-byte offsets of the subsequence) match the oracle run on the
+    window of keys each row reaches (the same keys lie inside and outside [0, L), so
+    the same rows and zero/masked entries enter its softmax)."""
+    b, l, w, dil, scale = 1, (1 << 25) + 4096, 3, 2, 0.05
+    say("band over 4 GiB", b, l, w, dil, "mask" if mask else "no mask")
+    q = synth.device_integer_tensor((b, l, 64), 6300, DEV)
+    k = synth.device_integer_tensor((b, l, 64), 6301, DEV)
+    v = synth.device_integer_tensor((b, l, 64), 6302, DEV)
+    o = ol.banded_bmm(q, k, v, w, dil, scale, mask_invalid=mask)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(6303)
+    rows = sorted(set([0, 1, 5, l - 1, l - 2, l - 7, (1 << 24) - 1, 1 << 24, (1 << 24) + 1,
+                       (1 << 25) - 2, (1 << 25) - 1, 1 << 25, (1 << 25) + 1]
+                      + rng.integers(0, l, 40).tolist()))
+    for i in rows:
+        lo, hi = max(0, i - w * dil), min(l, i + w * dil + 1)
+        win = [t[:, lo:hi].float().cpu() for t in (q, k, v)]
+        _, _, ref = oracle.band(*win, w, dil, scale, mask, rows=[i - lo], want_s=False,
+                                want_p=False)
+        got = o[0, i].cpu().numpy()
+        assert np.isfinite(got).all()
+        assert err(got, ref.reshape(got.shape)) <= TOL_BF16, i
+    del q, k, v, o
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("scale", [0.0, -0.3])
