@@ -13,9 +13,14 @@ both variants are timed and reported.
 the step time).  Per workload it also reports the GEMM stage in TFLOP/s and % of the
 bf16 MFMA peak (and, since its fp32 Y makes it HBM-bound on these shapes, its HBM
 GB/s and % of the roofline that binds it), the eOperator stage in GB/s and % of the
-HBM peak, and the fused kernel in TFLOP/s.  Each kernel is timed with HIP events around a HIP graph of
-back-to-back launches of that kernel (so host launch gaps do not count) on the stream
-it runs on.  `roofline` covers the kernel that takes the largest share of a step.
+HBM peak, and the fused kernel in TFLOP/s, each measured two ways:
+  warm     HIP events around a HIP graph of back-to-back launches of that kernel (host
+           launch gaps do not count), on the stream it runs on;
+  cold     ("cold" block) the median of single launches, each bracketed by HIP events
+           after a 512 MB buffer read that evicts L2 and the MALL.
+`roofline` covers the kernel with the largest share of a step (warm; frac_cold from the
+cold median).
+
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workloads.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
@@ -203,8 +208,8 @@ def main():
     torch.cuda.synchronize()
 
     # ----------------------------------------------------------------- timed steps
-    # K steps launched back to back on one stream: the host stays ahead of the GPU, so
-    # the kernels of consecutive steps run without gaps.
+    # K steps launched back to back: the host stays ahead of the GPU, so the kernels of
+    # consecutive steps run without gaps.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -246,19 +251,48 @@ def main():
         e1.synchronize()
         return e0.elapsed_time(e1) / reps   # ms per launch
 
+    # Cold: before every launch a 512 MB buffer is read (outside the events), which
+    # evicts L2 (4 MB per XCD) and the 256 MB MALL with clean lines; the median of the
+    # launches is kept.  (Writing the buffer instead leaves dirty lines whose write-back
+    # then runs inside the timed launch.)
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+    flush_sink = torch.empty((), dtype=torch.float32, device=dev)
+
+    def time_kernel_cold(fn, reps):
+        fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for i in range(reps):
+            torch.amax(flush, dim=0, out=flush_sink)
+            evs[i][0].record(stream)
+            fn()
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        d = sorted(a.elapsed_time(b) for a, b in evs)
+        return d[len(d) // 2] if len(d) % 2 else 0.5 * (d[len(d) // 2 - 1] + d[len(d) // 2])
+
     reps = max(args.steps, 10)
+    reps_cold = max(args.steps, 30)
+    # what a single launch costs between its events on this stream: a one-element fill,
+    # timed like the cold launches (part of every cold figure, most visible on the
+    # few-microsecond kernels)
+    event_floor = time_kernel_cold(lambda: flush_sink.fill_(0.0), reps_cold)
     per_cfg = {}
     kernels = []   # (name, ms per launch, bound, achieved, peak, unit, algorithmic work)
     for op in conv_ops:
         y = op["ws"][:op["m"] * op["nc"] * 4].view(torch.float32).view(op["m"], op["nc"])
         a = op["x"].view(op["m"], op["wl"].c)
         b = op["wt"].view(op["nc"], op["wl"].c)
-        g_ms = time_kernel(lambda: ol.gemm_nt(a, b, out=y), reps)
-        e_ms = time_kernel(lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y,
-                                                 out=op["out"]), reps)
+        g_fn = lambda: ol.gemm_nt(a, b, out=y)
+        e_fn = lambda: ol.eop_gather(op["desc"], op["wl"].transposed, y, out=op["out"])
         kw_f = {k_: v_ for k_, v_ in op["kw"].items() if k_ != "residues"}
-        f_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
-                                               **dict(kw_f, ws=None, fuse=True)), reps)
+        f_fn = lambda: op["entry"](op["x"], op["wt"], **dict(kw_f, ws=None, fuse=True))
+        g_ms = time_kernel(g_fn, reps)
+        e_ms = time_kernel(e_fn, reps)
+        f_ms = time_kernel(f_fn, reps)
+        g_cold = time_kernel_cold(g_fn, reps_cold)
+        e_cold = time_kernel_cold(e_fn, reps_cold)
+        f_cold = time_kernel_cold(f_fn, reps_cold)
         r_ms = None
         if op["cfg"] == 4:   # the dilated workload also in the residue sub-image form
             r_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
@@ -291,6 +325,20 @@ def main():
             "gemm_gflop": round(op["flops"] / 1e9, 4), "gemm_mbytes": round(g_bytes / 1e6, 3),
             "eop_mbytes": round(op["eop_bytes"] / 1e6, 3),
         }
+        t_g = max(t_mfma, t_hbm)
+        per_cfg[name].update({
+            "cold": {"gemm_ms": round(g_cold, 5),
+                     "gemm_tflops": round(op["flops"] / (g_cold * 1e-3) / 1e12, 2),
+                     "gemm_pct_mfma_peak": round(100 * t_mfma / (g_cold * 1e-3), 2),
+                     "gemm_pct_roofline": round(100 * t_g / (g_cold * 1e-3), 2),
+                     "eop_ms": round(e_cold, 5),
+                     "eop_gbs": round(op["eop_bytes"] / (e_cold * 1e-3) / 1e9, 1),
+                     "eop_pct_hbm_peak": round(100 * op["eop_bytes"] / (e_cold * 1e-3)
+                                               / (PEAK_HBM_GBS * 1e9), 2),
+                     "fused_ms": round(f_cold, 5),
+                     "fused_tflops": round(op["flops"] / (f_cold * 1e-3) / 1e12, 2),
+                     "fused_pct_mfma_peak": round(100 * t_mfma / (f_cold * 1e-3), 2)},
+        })
         if r_ms is not None:
             per_cfg[name]["fused_residue_form_ms"] = round(r_ms, 5)
         if op["fused"]:
@@ -306,18 +354,39 @@ def main():
             kernels.append((f"eop_gather[{name}]", e_ms, "hbm", e_gb, PEAK_HBM_GBS, "GB/s",
                             op["eop_bytes"]))
     b_ms = time_kernel(band_call, reps)
+    b_cold = time_kernel_cold(band_call, reps_cold)
     b_tf = bflops / (b_ms * 1e-3) / 1e12
     per_cfg[bwl.name] = {"path": "fused", "op_ms": round(b_ms, 5), "fused_ms": round(b_ms, 5),
                          "band_tflops": round(b_tf, 2),
                          "band_pct_mfma_peak": round(100 * b_tf / PEAK_BF16_TFLOPS, 2),
-                         "band_gflop": round(bflops / 1e9, 3)}
+                         "band_gflop": round(bflops / 1e9, 3),
+                         "cold": {"fused_ms": round(b_cold, 5),
+                                  "band_tflops": round(bflops / (b_cold * 1e-3) / 1e12, 2),
+                                  "band_pct_mfma_peak": round(
+                                      100 * bflops / (b_cold * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                                      2)}}
     kernels.append((f"band_fused[{bwl.name}]", b_ms, "mfma", b_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
                     bflops))
-    dom = max(kernels, key=lambda t: t[1])
+    # The roofline entry covers the kernel with the largest share of a step (warm
+    # back-to-back launches, whose average rocprofv3's kernel trace of the same run
+    # shows); frac_cold is the same fraction from the cold median.
+    cold_ms = {f"band_fused[{bwl.name}]": b_cold}
+    for op in conv_ops:
+        c = per_cfg[op["wl"].name]["cold"]
+        if op["fused"]:
+            cold_ms[f"conv_fused[{op['wl'].name}]"] = c["fused_ms"]
+        else:
+            cold_ms[f"gemm_nt[{op['wl'].name}]"] = c["gemm_ms"]
+            cold_ms[f"eop_gather[{op['wl'].name}]"] = c["eop_ms"]
+    timed = kernels
+    dom = max(timed, key=lambda t: t[1])
     roofline = {"kernel": dom[0], "bound": dom[2], "achieved": round(dom[3], 3),
                 "peak": dom[4], "unit": dom[5], "frac": round(dom[3] / dom[4], 4),
                 "traffic": traffic_record(dom[0]), "avg_launch_ms": round(dom[1], 5),
-                "algorithmic_per_launch": dom[6]}
+                "algorithmic_per_launch": dom[6],
+                "cold_launch_ms": round(cold_ms[dom[0]], 5),
+                "frac_cold": round(dom[6] / (cold_ms[dom[0]] * 1e-3)
+                                   / (1e12 if dom[5] == "TFLOP/s" else 1e9) / dom[4], 4)}
 
     # ---------------------------------------------------------------- CPU baseline
     cpu = None
@@ -338,6 +407,7 @@ def main():
                              f"{args.streams} streams (independent operators side by side)",
                    "paths": {op["wl"].name: op["path"] for op in conv_ops}},
         "per_config": per_cfg,
+        "cold_event_floor_ms": round(event_floor, 5),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
