@@ -27,7 +27,9 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
        python bench.py --stage NAME [--steps K]   (launch one stage kernel K times, for
        profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg>, fused:<cfg> for cfg 2-4, fusedres:4
        (the dilated workload as residue sub-image convolutions), band_fused,
-       band_g2bmm, band_softmax, band_gbmm, or copy = a plain 256 MiB device copy)
+       band_g2bmm, band_softmax, band_gbmm, srcnn_direct_fused, srcnn_split3x3,
+       srcnn_direct_staged (the SRCNN conv5x5 workload), or copy = a plain 256 MiB
+       device copy)
 """
 from __future__ import annotations
 
@@ -97,6 +99,34 @@ def conv_costs(wl, ho, wo, y_bytes=4, out_bytes=4):
         * valid_taps_1d(wl.w, wo, wl.s, wl.stride[1], wl.pad[1], wl.dil[1], wl.transposed)
     eop_bytes = taps * wl.k * y_bytes + wl.n * ho * wo * wl.k * out_bytes
     return flops, eop_bytes
+
+
+def srcnn_calls(dev):
+    """The SRCNN conv5x5 workload's inputs in HBM and its three derived programs, each
+    with preallocated outputs and workspaces: direct fused, split into 3x3 blocks
+    (fused 3x3 stage), direct GEMM + OffsetAdd."""
+    import torch
+    import paper_2208_02025_amd as ol
+    import synth
+    wl = synth.WORKLOADS[6]
+    x, wt = (t.to(dev) for t in synth.conv_inputs(wl))
+    desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), wl.stride, wl.pad, 1, 0, x.dtype,
+                        torch.float32)
+    out = torch.empty((wl.n, wl.h, wl.w, wl.k), dtype=torch.float32, device=dev)
+
+    def ws(flags):
+        return torch.empty(max(ol.conv_workspace_bytes(desc, False, flags), 16),
+                           dtype=torch.uint8, device=dev)
+    ws_split = ws(ol.CONV_SPLIT_3X3 | ol.FUSE_EPILOGUE)
+    ws_staged = ws(0)
+    fns = {
+        "direct_fused": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out, fuse=True),
+        "split3x3": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out, ws=ws_split,
+                                              fuse=True, split3x3=True),
+        "direct_staged": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out,
+                                                   ws=ws_staged),
+    }
+    return wl, fns
 
 
 def band_flops(wl):
@@ -367,6 +397,24 @@ def main():
                                       2)}}
     kernels.append((f"band_fused[{bwl.name}]", b_ms, "mfma", b_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
                     bflops))
+    # ------------------------- the Conv5x5 -> Conv3x3 derived form (a workload of its own,
+    # not part of the step): the SRCNN layer direct (fused over its 25 taps), in the
+    # split form (weight split + fused 3x3 stage with 4K channels + block OffsetAdd),
+    # and direct through GEMM + OffsetAdd; rates use the direct form's flops
+    next_rows = {}
+    swl, s_fns = srcnn_calls(dev)
+    s_flops = conv_costs(swl, swl.h, swl.w)[0]
+    row = {"row": "Conv5x5 -> Conv3x3 derived form", "gflop": round(s_flops / 1e9, 3),
+           "split_mfma_work_ratio": round(9 * ((swl.r + 2) // 3) * ((swl.s + 2) // 3)
+                                          / (swl.r * swl.s), 4)}
+    for nm, fn in s_fns.items():
+        w_ms = time_kernel(fn, reps)
+        c_ms = time_kernel_cold(fn, reps_cold)
+        row[f"{nm}_ms"] = round(w_ms, 5)
+        row[f"{nm}_tflops"] = round(s_flops / (w_ms * 1e-3) / 1e12, 2)
+        row[f"{nm}_cold_ms"] = round(c_ms, 5)
+    next_rows[swl.name] = row
+
     # The roofline entry covers the kernel with the largest share of a step (warm
     # back-to-back launches, whose average rocprofv3's kernel trace of the same run
     # shows); frac_cold is the same fraction from the cold median.
@@ -407,6 +455,7 @@ def main():
                              f"{args.streams} streams (independent operators side by side)",
                    "paths": {op["wl"].name: op["path"] for op in conv_ops}},
         "per_config": per_cfg,
+        "next_rows": next_rows,
         "cold_event_floor_ms": round(event_floor, 5),
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -439,6 +488,8 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
             fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=True))
         elif kind == "fusedres":
             fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], ws=None, residues=True))
+    elif name in ("srcnn_direct_fused", "srcnn_split3x3", "srcnn_direct_staged"):
+        fn = srcnn_calls(q.device)[1][name[len("srcnn_"):]]
     elif name == "band_fused":
         fn = lambda: ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale,
                                    mask_invalid=bwl.mask_invalid, out=o)

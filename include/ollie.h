@@ -62,6 +62,7 @@ typedef enum {
 #define OLLIE_BAND_STAGED       (1u << 2)  /* band: three kernels through S and P in the workspace */
 #define OLLIE_BAND_MASK_INVALID (1u << 3)  /* band: keys outside [0,l) are left out of the softmax */
 #define OLLIE_DILATED_RESIDUES  (1u << 4)  /* dilated conv: as non-dilated convs over residue sub-images */
+#define OLLIE_CONV_SPLIT_3X3    (1u << 5)  /* conv: as a 3x3 convolution over kernel blocks + OffsetAdd */
 
 /* Geometry of a convolution-family operator.
  *   X   [n][h][w][c]   input (NHWC).  As a GEMM operand it is A'[m][c] with
@@ -134,7 +135,9 @@ int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, 
 /* Bytes of workspace that derived_conv2d / derived_dilated_conv2d /
  * derived_conv_transpose2d need: the instantiated scope Y [n*h*w][r*s*k] in fp32
  * (or bf16 with OLLIE_Y_BF16); 0 when OLLIE_FUSE_EPILOGUE is set and the fused kernel
- * covers the shape.  Returns 0 for invalid geometry. */
+ * covers the shape.  With OLLIE_CONV_SPLIT_3X3 (derived_conv2d): the split weights,
+ * the 3x3 stage Z and that stage's own workspace (see derived_conv2d).  Returns 0 for
+ * invalid geometry. */
 size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags);
 
 /* Bytes of workspace banded_bmm needs: 0 for the fused path; with OLLIE_BAND_STAGED,
@@ -167,7 +170,27 @@ const char* ollie_version(void);
  * c % 64 == 0, at most 64 taps and, for the transposed operator, at most 16 stride
  * residue classes; other shapes take the two-stage path, which needs the workspace.
  * Summation order differs from the two-stage path, so fp32 results agree to rounding
- * (integer-valued inputs agree exactly). */
+ * (integer-valued inputs agree exactly).
+ *
+ * OLLIE_CONV_SPLIT_3X3 evaluates the derived form that turns an R x S convolution into
+ * a 3x3 one (the Conv5x5 -> Conv3x3 transformation of section 6, Table 3), stride 1
+ * only.  Boundary relaxing extends the kernel to 3*nbr x 3*nbs taps (nbr = ceil(R/3),
+ * nbs = ceil(S/3)) with zero weights; variable substitution writes r = 3*a + r',
+ * s = 3*b + s'; summation splitting instantiates the inner sum over (r', s', c) as a
+ * 3x3 convolution with nbr*nbs*K output channels,
+ *   W3[r'][s'][(a*nbs + b)*K + k][c] = Wt[3a + r'][3b + s'][k][c]  (0 outside R x S)
+ *   Z[n][i][j][(a*nbs + b)*K + k] = sum_{r',s',c} X0[n][i - ph - er + r'][j - pw - es + s'][c]
+ *                                                 * W3[r'][s'][(a*nbs + b)*K + k][c]
+ * (X0: X zero outside the image; er = 3*nbr - R, es = 3*nbs - S; Z is that
+ * convolution with padding ph + er, pw + es, so i < h + 2(ph + er) - 2), and the outer
+ * sum over the kernel blocks is an OffsetAdd with offset step 3:
+ *   out[n][ho][wo][k] = sum_{a < nbr, b < nbs} Z[n][ho + er + 3a][wo + es + 3b][(a*nbs + b)*K + k].
+ * Kernels: the weight split, the 3x3 stage (fused with OLLIE_FUSE_EPILOGUE when the
+ * fused kernel covers it, else GEMM + OffsetAdd, whose Y honours OLLIE_Y_BF16), the
+ * block OffsetAdd (which takes the element-wise tail).  ws holds, each at a 256-byte
+ * aligned offset: W3 [3][3][nbr*nbs*K][c] in in_dtype, Z in fp32, then the 3x3
+ * stage's scope Y when that stage is not fused.  Needs stride 1 and dilation 1, else
+ * OLLIE_EINVAL. */
 int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                    void* ws, size_t ws_bytes, uint32_t flags, void* stream);
 

@@ -8,6 +8,11 @@ module evaluates the *derived* expression the method reaches, in float64 NumPy:
   Eq. (3) and Eq. (4) -- and an outer eOperator that sums the partials of Y over
   (r,s) through the substituted indices (the OffsetAdd of section 2; the selective
   add of section 6.3 for the transposed case);
+* the R x S -> 3x3 rewrite (Conv5x5 -> Conv3x3, section 6 / Table 3): the tap range
+  is relaxed to whole 3x3 blocks with zero weights (boundary relaxing), the tap index
+  substituted as r = 3a + r' (variable substitution), and the sum split into an inner
+  3x3 convolution over (r', s', c) with one output-channel group per block (a, b) and
+  an outer OffsetAdd over the blocks with offset step 3 (summation splitting);
 * banded matmul: the dilated band is split by residue i mod dil into non-dilated
   bands over strided subsequences (the dilated-to-non-dilated G2BMM rewrite of
   section 6.4), each evaluated with dense matrix products, then re-interleaved.
@@ -99,6 +104,43 @@ def derived_conv2d(x, wt, stride, pad, dil):
 def derived_conv_transpose2d(x, wt, stride, pad, dil, out_pad=(0, 0)):
     y = gemm_stage(x, wt)
     return selective_add(y, x.shape, wt.shape, stride, pad, dil, out_pad)
+
+
+def split_weights_3x3(wt):
+    """W3[r'][s'][(a*nbs + b)*K + k][c] = Wt[3a + r'][3b + s'][k][c], zero where the
+    block overhangs the R x S kernel (the relaxed taps)."""
+    r_n, s_n, k, c = wt.shape
+    nbr, nbs = -(-r_n // 3), -(-s_n // 3)
+    w6 = np.zeros((3 * nbr, 3 * nbs, k, c), dtype=np.float64)
+    w6[:r_n, :s_n] = wt
+    w3 = np.zeros((3, 3, nbr * nbs * k, c), dtype=np.float64)
+    for a in range(nbr):
+        for b in range(nbs):
+            g = a * nbs + b
+            w3[:, :, g * k:(g + 1) * k, :] = w6[3 * a:3 * a + 3, 3 * b:3 * b + 3]
+    return w3
+
+
+def derived_conv2d_split3x3(x, wt, pad):
+    """Stride-1, dilation-1 convolution in the 3x3 derived form: the inner 3x3 stage
+    (itself GEMM + OffsetAdd) with padding pad + er, then the block OffsetAdd
+    out[ho][wo][k] = sum_{a,b} Z[ho + er + 3a][wo + es + 3b][(a*nbs + b)*K + k]."""
+    n_, h, w, _ = x.shape
+    r_n, s_n, k, _ = wt.shape
+    ph, pw = pad
+    nbr, nbs = -(-r_n // 3), -(-s_n // 3)
+    er, es = 3 * nbr - r_n, 3 * nbs - s_n
+    w3 = split_weights_3x3(wt)
+    z = derived_conv2d(x, w3, (1, 1), (ph + er, pw + es), (1, 1))   # [n, hz, wz, nbr*nbs*K]
+    ho_n = conv_out_size(h, r_n, 1, ph, 1)
+    wo_n = conv_out_size(w, s_n, 1, pw, 1)
+    out = np.zeros((n_, ho_n, wo_n, k), dtype=np.float64)
+    for a in range(nbr):
+        for b in range(nbs):
+            g = a * nbs + b
+            out += z[:, er + 3 * a:er + 3 * a + ho_n, es + 3 * b:es + 3 * b + wo_n,
+                     g * k:(g + 1) * k]
+    return out
 
 
 def _band_nondilated(q, k, v, w, scale, mask, l_full_in_range):

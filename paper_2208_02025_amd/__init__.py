@@ -27,6 +27,7 @@ Y_BF16 = 1 << 1
 BAND_STAGED = 1 << 2
 BAND_MASK_INVALID = 1 << 3
 DILATED_RESIDUES = 1 << 4
+CONV_SPLIT_3X3 = 1 << 5
 
 _STATUS_NAMES = {OK: "OLLIE_OK", EINVAL: "OLLIE_EINVAL", EDTYPE: "OLLIE_EDTYPE",
                  EWORKSPACE: "OLLIE_EWORKSPACE", EALIGN: "OLLIE_EALIGN", EHIP: "OLLIE_EHIP"}
@@ -225,12 +226,16 @@ def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output
 
 
 def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=False,
-                   out=None, ws=None, fuse=False, bias=None, residual=None, relu=False):
+                   out=None, ws=None, fuse=False, bias=None, residual=None, relu=False,
+                   split3x3=False):
     """Conv2d (dilation 1) as GEMM + OffsetAdd eOperator (fuse=True: the fused
     expression, no Y).  x [N,H,W,C], wt [R,S,K,C].  bias / residual / relu: an
-    element-wise tail act(conv + bias + residual) evaluated in the last kernel."""
+    element-wise tail act(conv + bias + residual) evaluated in the last kernel.
+    split3x3=True (stride 1): the R x S kernel as ceil(R/3) x ceil(S/3) blocks of a 3x3
+    convolution (fused by `fuse` where covered) whose partial outputs an OffsetAdd with
+    offset step 3 sums (the Conv5x5 -> Conv3x3 derived form)."""
     return _conv("derived_conv2d", False, x, wt, stride, padding, 1, 0, out_dtype, y_bf16,
-                 out, ws, fuse, bias, residual, relu)
+                 out, ws, fuse, bias, residual, relu, CONV_SPLIT_3X3 if split3x3 else 0)
 
 
 def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJ_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libollie.so")
-SOURCES = ["abi.hip", "gemm.hip", "eop.hip", "band.hip", "conv_fused.hip"]
+SOURCES = ["abi.hip", "gemm.hip", "eop.hip", "band.hip", "conv_fused.hip", "split3.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 ops are disabled for all device code (the host pass warns that it does

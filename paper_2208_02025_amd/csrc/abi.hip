@@ -102,11 +102,70 @@ bool fused_path(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo
            conv_fused_supported(conv_geom(d, ho, wo), conv_form(transposed, flags));
 }
 
-size_t conv_ws(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
-               uint32_t flags) {
+size_t conv_ws_plain(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
+                     uint32_t flags) {
     if (fused_path(d, transposed, ho, wo, flags)) return 0;
     return (size_t)(d->n * d->h * d->w) * (size_t)(d->r * d->s * d->k) *
            ((flags & OLLIE_Y_BF16) ? 2 : 4);
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The R x S -> 3x3 derived form (OLLIE_CONV_SPLIT_3X3): kernel blocks nbr x nbs, the
+// relaxed taps er, es, and the 3x3 stage as a convolution descriptor X -> Z.
+struct Split3 {
+    int64_t nbr, nbs, er, es;
+    ollie_conv_desc d3;
+};
+
+Split3 split3_of(const ollie_conv_desc* d) {
+    Split3 q;
+    q.nbr = (d->r + 2) / 3;
+    q.nbs = (d->s + 2) / 3;
+    q.er = 3 * q.nbr - d->r;
+    q.es = 3 * q.nbs - d->s;
+    q.d3 = *d;
+    q.d3.k = q.nbr * q.nbs * d->k;
+    q.d3.r = 3;
+    q.d3.s = 3;
+    q.d3.pad_h = d->pad_h + (int32_t)q.er;
+    q.d3.pad_w = d->pad_w + (int32_t)q.es;
+    q.d3.out_dtype = OLLIE_F32;
+    return q;
+}
+
+// Checks the split form's extra conditions; fills the 3x3 stage's output size.
+int check_split3(const ollie_conv_desc* d, int transposed, const Split3& q, int64_t* hz,
+                 int64_t* wz) {
+    if (transposed) return fail(OLLIE_EINVAL, "OLLIE_CONV_SPLIT_3X3 applies to derived_conv2d");
+    if (d->stride_h != 1 || d->stride_w != 1 || d->dil_h != 1 || d->dil_w != 1)
+        return fail(OLLIE_EINVAL, "OLLIE_CONV_SPLIT_3X3 needs stride 1 and dilation 1");
+    if (d->pad_h > (1 << 28) || d->pad_w > (1 << 28) || d->r > (1 << 28) || d->s > (1 << 28))
+        return fail(OLLIE_EINVAL, "sizes overflow 32-bit arithmetic");
+    int st = check_conv_geom(&q.d3, 0, hz, wz);
+    if (st) return st;
+    if (mul(mul(mul(d->k, 9), q.nbr * q.nbs), d->c) >= kMaxElems)
+        return fail(OLLIE_EINVAL, "split weights must have < 2^31 elements");
+    return OLLIE_OK;
+}
+
+size_t split3_ws(const ollie_conv_desc* d, const Split3& q, int64_t hz, int64_t wz,
+                 uint32_t flags) {
+    const size_t el = d->in_dtype == OLLIE_BF16 ? 2 : 4;
+    const size_t w3 = (size_t)9 * (size_t)q.d3.k * (size_t)d->c * el;
+    const size_t z = (size_t)(d->n * hz * wz) * (size_t)q.d3.k * 4;
+    return align256(w3) + align256(z) + conv_ws_plain(&q.d3, 0, hz, wz, flags);
+}
+
+size_t conv_ws(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
+               uint32_t flags) {
+    if (flags & OLLIE_CONV_SPLIT_3X3) {
+        const Split3 q = split3_of(d);
+        int64_t hz, wz;
+        if (check_split3(d, transposed, q, &hz, &wz)) return 0;
+        return split3_ws(d, q, hz, wz, flags & ~(uint32_t)OLLIE_CONV_SPLIT_3X3);
+    }
+    return conv_ws_plain(d, transposed, ho, wo, flags);
 }
 
 int check_gemm(int64_t m, int64_t n, int64_t k, const void* a, const void* b, const void* y,
@@ -141,6 +200,60 @@ int make_epi(const ollie_conv_epilogue* e, Epi* out) {
 
 int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
                 void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                const ollie_conv_epilogue* epilogue, void* stream);
+
+// The R x S -> 3x3 derived form: weight split, the 3x3 stage into Z (fp32), then the
+// OffsetAdd over the kernel blocks (taps spaced 3 apart in Z, shifted by er, es),
+// which carries the element-wise tail.
+int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
+                void* out, void* ws, size_t ws_bytes, uint32_t flags, const Epi& epi,
+                int64_t ho, int64_t wo, void* stream) {
+    const Split3 q = split3_of(d);
+    int64_t hz, wz;
+    int st = check_split3(d, transposed, q, &hz, &wz);
+    if (st) return st;
+    const size_t need = split3_ws(d, q, hz, wz, flags);
+    if (!ws) return fail(OLLIE_EINVAL, "null workspace pointer (the split form needs W3 and Z)");
+    if (ws_bytes < need)
+        return fail(OLLIE_EWORKSPACE, "workspace too small: need %zu bytes, got %zu", need,
+                    ws_bytes);
+    if (!aligned16(x) || !aligned16(wt) || !aligned16(out) || !aligned16(ws))
+        return fail(OLLIE_EALIGN, "tensor and workspace pointers must be 16-byte aligned");
+    const size_t el = d->in_dtype == OLLIE_BF16 ? 2 : 4;
+    const size_t w3_bytes = align256((size_t)9 * (size_t)q.d3.k * (size_t)d->c * el);
+    const size_t z_bytes = align256((size_t)(d->n * hz * wz) * (size_t)q.d3.k * 4);
+    char* w3 = static_cast<char*>(ws);
+    char* z = w3 + w3_bytes;
+    char* inner = z + z_bytes;
+    // everything the 3x3 stage checks, before the first launch
+    if (!fused_path(&q.d3, 0, hz, wz, flags)) {
+        st = check_gemm(d->n * d->h * d->w, 9 * q.d3.k, d->c, x, w3, inner, d->in_dtype,
+                        (flags & OLLIE_Y_BF16) ? OLLIE_BF16 : OLLIE_F32);
+        if (st) return st;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = launch_split_weights_3x3(conv_geom(d, ho, wo), wt, w3,
+                                            d->in_dtype == OLLIE_BF16, s);
+    if (e != hipSuccess) return hip_fail(e, "weight split launch");
+    st = conv_common(&q.d3, 0, x, w3, z, inner, ws_bytes - w3_bytes - z_bytes, flags, nullptr,
+                     stream);
+    if (st) return st;
+    ConvGeom gb = conv_geom(d, ho, wo);
+    gb.h = hz;
+    gb.w = wz;
+    gb.r = q.nbr;
+    gb.s = q.nbs;
+    gb.ph = -(int32_t)q.er;
+    gb.pw = -(int32_t)q.es;
+    gb.dh = 3;
+    gb.dw = 3;
+    e = launch_eop_gather(gb, 0, z, 0, out, d->out_dtype == OLLIE_BF16, epi, s);
+    if (e != hipSuccess) return hip_fail(e, "block OffsetAdd launch");
+    return OLLIE_OK;
+}
+
+int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
+                void* out, void* ws, size_t ws_bytes, uint32_t flags,
                 const ollie_conv_epilogue* epilogue, void* stream) {
     int64_t ho, wo;
     int st = check_conv_geom(d, transposed, &ho, &wo);
@@ -148,11 +261,19 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     Epi epi;
     st = make_epi(epilogue, &epi);
     if (st) return st;
-    if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE | OLLIE_DILATED_RESIDUES))
+    if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE | OLLIE_DILATED_RESIDUES |
+                            OLLIE_CONV_SPLIT_3X3))
         return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
     if (!x || !wt || !out) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!dtype_ok(d->in_dtype) || !dtype_ok(d->out_dtype))
         return fail(OLLIE_EDTYPE, "in_dtype/out_dtype must be OLLIE_F32 or OLLIE_BF16");
+    if (flags & OLLIE_CONV_SPLIT_3X3) {
+        if (flags & OLLIE_DILATED_RESIDUES)
+            return fail(OLLIE_EINVAL, "OLLIE_CONV_SPLIT_3X3 and OLLIE_DILATED_RESIDUES exclude "
+                                      "each other");
+        return conv_split3(d, transposed, x, wt, out, ws, ws_bytes,
+                           flags & ~(uint32_t)OLLIE_CONV_SPLIT_3X3, epi, ho, wo, stream);
+    }
     if ((flags & OLLIE_DILATED_RESIDUES) && !fused_path(d, transposed, ho, wo, flags))
         return fail(OLLIE_EINVAL,
                     "OLLIE_DILATED_RESIDUES needs OLLIE_FUSE_EPILOGUE, stride 1, bf16 inputs, "
@@ -265,6 +386,8 @@ int derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const 
                               void* out, void* ws, size_t ws_bytes, uint32_t flags,
                               const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
+    if (flags & OLLIE_CONV_SPLIT_3X3)
+        return fail(OLLIE_EINVAL, "OLLIE_CONV_SPLIT_3X3 applies to derived_conv2d");
     return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
 }
 

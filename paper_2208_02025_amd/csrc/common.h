@@ -159,6 +159,11 @@ bool conv_fused_supported(const ConvGeom& g, int form);
 hipError_t launch_conv_fused(const ConvGeom& g, int form, const void* x, const void* wt,
                              void* out, int out_bf16, const Epi& epi, hipStream_t stream);
 
+// Weight blocks of the R x S -> 3x3 derived form: W3 [3][3][ceil(R/3)*ceil(S/3)*K][C]
+// from Wt [R][S][K][C] (g.r, g.s, g.k, g.c), zero where a block overhangs the kernel.
+hipError_t launch_split_weights_3x3(const ConvGeom& g, const void* wt, void* w3, int bf16,
+                                    hipStream_t stream);
+
 struct BandGeom {
     int64_t b, l, d, w;
     int32_t dil;

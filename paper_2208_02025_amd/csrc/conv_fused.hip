@@ -732,9 +732,20 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
     if (P.x_bytes == 0 || P.w_bytes == 0) return go<128, 128, 2, OT, 8, false>(P, x, wt, out, epi, st);
     int cfg = forced;
     if (cfg == 9 && !window_ok(P)) cfg = -1;
-    if (cfg < 0 || cfg > 12) {
+    if (cfg < 0 || cfg > 14) {
         FusedPlan tmp = P;
-        if (plan_tiles(tmp, 192, 128) >= 240) cfg = 10;
+        // k-tiles of the longest class contraction
+        int steps = 0;
+        for (int c = 0; c < P.ncls; ++c) {
+            const int n = P.cls_th[c].n * P.cls_tw[c].n * (P.c / kTileK);
+            steps = n > steps ? n : steps;
+        }
+        // output-channel tiles no wider than K (a wider tile multiplies padding)
+        if (P.k <= 32 && plan_tiles(tmp, 128, 32) >= 240) cfg = 13;
+        else if (P.k <= 64) cfg = 12;
+        // a short contraction: the k split's final reduction does not pay
+        else if (steps < 16 && plan_tiles(tmp, 128, 128) >= 240) cfg = 1;
+        else if (plan_tiles(tmp, 192, 128) >= 240) cfg = 10;
         else if (plan_tiles(tmp, 128, 128) >= 240) cfg = 1;
         else if (plan_tiles(tmp, 64, 128) >= 240) cfg = 2;
         else cfg = 12;
@@ -753,6 +764,8 @@ hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, cons
     case 10: return go<192, 128, 2, OT, 8, true, 2>(P, x, wt, out, epi, st);
     case 11: return go<128, 128, 2, OT, 8, true, 2>(P, x, wt, out, epi, st);
     case 12: return go<64, 64, 4, OT, 8, true, 2>(P, x, wt, out, epi, st);
+    case 13: return go<128, 32, 4, OT, 4>(P, x, wt, out, epi, st);
+    case 14: return go<256, 32, 3, OT, 4>(P, x, wt, out, epi, st);
     // the small shapes run right after other kernels have evicted their operands: a
     // 4-deep copy ring hides the longer cold loads (measured in the benchmark step)
     default: return go_pipe<64, 64, 4, OT>(P, x, wt, out, epi, st);

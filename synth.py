@@ -67,7 +67,9 @@ class BandWorkload:
 # The five workloads, sized as the layers they stand in for:
 # 1: a tiny 3x3 conv (parity only); 2: a ResNet-18 stage-3 conv3x3 at batch 16;
 # 3: a DCGAN generator ConvTranspose2d; 4: a CSRNet back-end dilated conv;
-# 5: Longformer-base dilated sliding-window attention (8 sequences x 12 heads).
+# 5: Longformer-base dilated sliding-window attention (8 sequences x 12 heads);
+# 6: an SRCNN 9-5-5 second layer (conv5x5, 64 -> 32 channels, "same" padding) on a
+# 512x512 image, the workload of the Conv5x5 -> Conv3x3 derived form.
 WORKLOADS = {
     1: ConvWorkload(1, "conv3x3_tiny", "conv2d", n=1, c=16, h=14, w=14, k=16, r=3, s=3,
                     stride=(1, 1), pad=(1, 1), dtype="f32", x_dist="uniform", w_dist="uniform"),
@@ -82,6 +84,9 @@ WORKLOADS = {
                     dtype="bf16", x_dist="relu_normal", w_std=math.sqrt(2.0 / (9 * 512))),
     5: BandWorkload(5, "longformer_band_b96_l4096_d64_w256_dil2", b=96, l=4096, d=64, w=256,
                     dilation=2, scale=1.0, mask_invalid=False, dtype="bf16"),
+    6: ConvWorkload(6, "srcnn_conv5x5_c64_k32_512x512", "conv2d", n=1, c=64, h=512, w=512,
+                    k=32, r=5, s=5, stride=(1, 1), pad=(2, 2), dtype="bf16",
+                    x_dist="relu_normal", w_std=math.sqrt(2.0 / (25 * 64))),
 }
 
 

@@ -257,6 +257,31 @@ def test_residue_flag_rejections(lib):
     assert ol.conv_workspace_bytes(d_ok, False, R) == 0
 
 
+def test_split3x3_flag_rejections_and_workspace(lib):
+    S = ol.CONV_SPLIT_3X3
+    d5 = conv(c=64, r=5, s=5, pad=2)
+    assert call_conv(lib, "derived_conv_transpose2d", conv(c=64, r=5, s=5, stride=2, pad=2),
+                     flags=S)[0] == ol.EINVAL
+    assert call_conv(lib, "derived_dilated_conv2d", d5, flags=S)[0] == ol.EINVAL
+    assert call_conv(lib, "derived_conv2d", conv(c=64, r=5, s=5, stride=2, pad=2),
+                     flags=S)[0] == ol.EINVAL
+    assert call_conv(lib, "derived_conv2d", d5, ws=None, flags=S)[0] == ol.EINVAL
+    assert call_conv(lib, "derived_conv2d", d5, ws_bytes=1000, flags=S)[0] == ol.EWORKSPACE
+    assert call_conv(lib, "derived_conv2d", conv(c=12, r=5, s=5, pad=2),
+                     flags=S)[0] == ol.EALIGN            # bf16 rows of 24 bytes
+    assert call_conv(lib, "derived_conv2d", d5, out=MIS, flags=S)[0] == ol.EALIGN
+    # W3 [3][3][4*16][64] bf16 + Z [1][18][18][64] fp32 + the 3x3 stage's Y (two-stage)
+    w3, z, y = 9 * 64 * 64 * 2, 18 * 18 * 64 * 4, 14 * 14 * 9 * 64 * 4
+    assert ol.conv_workspace_bytes(d5, False, S) == w3 + z + y
+    assert ol.conv_workspace_bytes(d5, False, S | ol.FUSE_EPILOGUE) == w3 + z
+    assert ol.conv_workspace_bytes(d5, False, S | ol.Y_BF16) == w3 + z + y // 2
+    assert ol.conv_workspace_bytes(d5, True, S) == 0
+    # a 4x2 kernel: blocks 2x1, relaxed taps er = 2, es = 1: Z is (14+2*3-2) x (14+2*2-2)
+    d42 = conv(c=64, r=4, s=2, pad=1)
+    assert ol.conv_workspace_bytes(d42, False, S | ol.FUSE_EPILOGUE) == \
+        9 * 32 * 64 * 2 + 18 * 16 * 32 * 4
+
+
 def test_validation_never_lets_a_bad_descriptor_through(lib):
     """Randomised descriptors with invalid fields: every call returns a non-zero status
     with a message before any HIP call (fake device pointers are never touched)."""

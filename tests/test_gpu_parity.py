@@ -216,6 +216,75 @@ def test_fused_conv_input_over_2gib_sampled():
     torch.cuda.empty_cache()
 
 
+# (n, c, h, w, k, r, s, pad, dtype): the R x S -> 3x3 derived form.  c % 64 == 0 bf16
+# cases take the fused 3x3 stage when fuse=True; the others its GEMM + OffsetAdd.
+SPLIT3_GPU_CASES = [
+    (2, 64, 13, 11, 24, 5, 5, (2, 2), "bf16"),
+    (1, 72, 9, 10, 20, 5, 5, (0, 0), "bf16"),
+    (1, 16, 8, 7, 12, 4, 2, (1, 3), "f32"),
+    (1, 64, 12, 12, 16, 7, 7, (3, 3), "bf16"),
+    (1, 64, 6, 6, 8, 3, 3, (1, 1), "bf16"),
+    (3, 128, 17, 9, 40, 5, 4, (2, 1), "bf16"),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(SPLIT3_GPU_CASES)))
+@pytest.mark.parametrize("fuse", [False, True])
+def test_split3x3_integer_exact(ci, fuse):
+    n, c, h, w, k, r, s, pad, dt = SPLIT3_GPU_CASES[ci]
+    say("split3x3", SPLIT3_GPU_CASES[ci], "fuse" if fuse else "staged")
+    x = synth.random_tensor((n, h, w, c), 11000 + ci, dt, integer=True)
+    wt = synth.random_tensor((r, s, k, c), 11100 + ci, dt, integer=True)
+    out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), 1, pad, fuse=fuse, split3x3=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(out), oracle.conv2d(x, wt, 1, pad, 1))
+
+
+@pytest.mark.parametrize("integer", [False, True])
+def test_srcnn_workload_direct_and_split_sampled(integer):
+    """The SRCNN conv5x5 workload at full size, direct (fused 25 taps) and in the 3x3
+    derived form (fused 3x3 stage + block OffsetAdd), on 4000 sampled outputs
+    (borders included) evaluated one by one by the oracle."""
+    wl = synth.WORKLOADS[6]
+    say("srcnn workload", "integer" if integer else "float")
+    x, wt = synth.conv_inputs(wl, integer=integer)
+    ho, wo = wl.h, wl.w
+    rng = np.random.default_rng(11300)
+    idx = rng.integers(0, wl.n * ho * wo * wl.k, 4000)
+    corners = [((i * ho + j) * wo + q) * wl.k + kk for i in range(wl.n) for j in (0, ho - 1)
+               for q in (0, 1, wo - 2, wo - 1) for kk in (0, wl.k - 1)]
+    idx = np.unique(np.concatenate([idx, np.array(corners)]))
+    ref = oracle.conv2d(x, wt, wl.stride, wl.pad, 1, idx=idx)
+    for split in (False, True):
+        out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), wl.stride, wl.pad, fuse=True,
+                                split3x3=split)
+        torch.cuda.synchronize()
+        got = to_np(out).reshape(-1)[idx]
+        if integer:
+            assert np.array_equal(got, ref), split
+        else:
+            assert err(got, ref) <= TOL_BF16, split
+
+
+def test_split3x3_float_tail_bf16_out_and_bf16_scope():
+    """Random bf16 inputs: the split form with bias + ReLU and a bf16 out, and with a
+    bf16 Y in its 3x3 stage, within the bf16 tolerance of the definition."""
+    n, c, h, w, k, r, s, pad = 2, 64, 15, 13, 32, 5, 5, (2, 2)
+    say("split3x3 float", n, c, h, w, k, r, s, pad)
+    x = synth.random_tensor((n, h, w, c), 11200, "bf16", dist="normal")
+    wt = synth.random_tensor((r, s, k, c), 11201, "bf16", dist="normal")
+    bias = synth.random_tensor((k,), 11202)
+    ref = oracle.conv2d(x, wt, 1, pad, 1)
+    out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), 1, pad, out_dtype=torch.bfloat16,
+                            fuse=True, split3x3=True, bias=bias.to(DEV), relu=True)
+    torch.cuda.synchronize()
+    assert out.dtype == torch.bfloat16
+    assert err(to_np(out), np.maximum(ref + bias.double().numpy(), 0.0)) <= TOL_BF16
+    out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), 1, pad, y_bf16=True, split3x3=True)
+    torch.cuda.synchronize()
+    assert err(to_np(out), ref) <= TOL_BF16
+
+
 GEMM_CONFIGS = 5
 
 
@@ -613,8 +682,11 @@ TILE_CASES = [
 ]
 
 
+FUSED_CONFIGS = 15
+
+
 @pytest.mark.parametrize("ci", range(len(TILE_CASES)))
-@pytest.mark.parametrize("cfg", range(13))
+@pytest.mark.parametrize("cfg", range(FUSED_CONFIGS))
 def test_every_tile_shape_integer_exact(cfg, ci, monkeypatch):
     kind, n, c, h, w, k, r, s, st, pd, dl, op, res = TILE_CASES[ci]
     say("tile shape", cfg, TILE_CASES[ci])

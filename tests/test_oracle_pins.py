@@ -220,6 +220,45 @@ def test_derived_form_convt_exact_on_integers(ci):
     assert np.array_equal(got, ref)
 
 
+# (n, c, h, w, k, r, s, pad): 5x5 with "same" and no padding, kernels that are not a
+# whole number of 3x3 blocks along one or both axes, one already 3x3, one 1x1, 7x7
+SPLIT3_CASES = [
+    (1, 3, 9, 8, 2, 5, 5, (2, 2)),
+    (2, 2, 8, 7, 3, 5, 5, (0, 0)),
+    (1, 2, 7, 9, 2, 4, 2, (1, 3)),
+    (1, 3, 6, 6, 2, 3, 3, (1, 1)),
+    (1, 2, 5, 5, 2, 1, 1, (0, 0)),
+    (1, 2, 10, 9, 2, 7, 6, (3, 2)),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(SPLIT3_CASES)))
+def test_split3x3_derived_form_exact_on_integers(ci):
+    """The R x S -> 3x3 derived form equals the convolution's definition exactly on
+    integer inputs (the rewrite only adds zero-weight taps and regroups the sum)."""
+    n, c, h, w, k, r, s, pad = SPLIT3_CASES[ci]
+    x = synth.random_tensor((n, h, w, c), 1200 + ci, integer=True).numpy()
+    wt = synth.random_tensor((r, s, k, c), 1300 + ci, integer=True).numpy()
+    got = dfm.derived_conv2d_split3x3(x, wt, pad)
+    ref = oracle.conv2d(x, wt, 1, pad, 1)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
+
+
+def test_split3x3_weights_cover_every_tap_once():
+    """Each tap of the kernel lands in exactly one (block, r', s') slot of W3 and the
+    relaxed slots are zero: the block sums of W3 reproduce the kernel's total per
+    (k, c), and the count of non-zero slots equals R*S on an all-ones kernel."""
+    wt = np.ones((5, 4, 2, 3))
+    w3 = dfm.split_weights_3x3(wt)
+    assert w3.shape == (3, 3, 2 * 2 * 2, 3)
+    assert int((w3 != 0).sum()) == 5 * 4 * 2 * 3
+    wr = synth.random_tensor((5, 4, 2, 3), 1400).numpy().astype(np.float64)
+    w3r = dfm.split_weights_3x3(wr)
+    tot = w3r.sum(axis=(0, 1)).reshape(4, 2, 3).sum(axis=0)
+    np.testing.assert_allclose(tot, wr.sum(axis=(0, 1)), rtol=0, atol=1e-12)
+
+
 @pytest.mark.parametrize("integer", [True, False])
 def test_tiny_workload_against_torch_and_derived_form(integer):
     wl = synth.WORKLOADS[1]
