@@ -1,0 +1,215 @@
+"""The host-side derivation engine (paper_2208_02025_amd.derive): every rule keeps an
+expression's value, fingerprints see through renaming and reordering, the search
+reaches the derived programs the kernels run, and the plans it emits are the
+geometry the C ABI takes.  CPU only; tiny integer shapes, evaluated by brute force
+and pinned to the oracle's definitions."""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2208_02025_amd import derive as D
+import paper_2208_02025_amd as ol
+
+
+def rand_inputs(prog, seed):
+    rng = np.random.default_rng(seed)
+    return {n: rng.integers(-3, 4, size=shp).astype(np.float64) for n, shp in prog.inputs}
+
+
+def value(prog, t):
+    arr, org = D.evaluate(prog, t)
+    assert all(o == 0 for o in org)
+    return arr
+
+
+PROGS = [
+    D.conv2d_expr(1, 2, 4, 3, 2, 3, 2, (1, 1), (1, 0), (1, 1)),
+    D.conv2d_expr(2, 1, 5, 4, 1, 2, 2, (2, 1), (1, 1), (1, 2)),
+    D.conv_transpose2d_expr(1, 2, 3, 2, 2, 3, 2, (2, 1), (1, 0), (1, 1), (1, 0)),
+    D.g2bmm_expr(1, 7, 2, 2, 2),
+]
+
+
+@pytest.mark.parametrize("pi", range(len(PROGS)))
+def test_every_rule_application_keeps_the_value(pi):
+    """All rule applications the search makes, two levels deep from the operator's
+    expression, evaluate to the same output on a random integer instance."""
+    prog = PROGS[pi]
+    t = rand_inputs(prog, 100 + pi)
+    ref = value(prog, t)
+    frontier = [prog]
+    kinds = set()
+    for _ in range(2):
+        nxt = []
+        for p in frontier:
+            for mv, q in D._moves(p):
+                kinds.add(mv[0])
+                assert np.array_equal(value(q, t), ref), mv
+                nxt.append(q)
+        frontier = nxt[:40]
+    # the band has a single summation iterator: no split applies to it
+    assert ("split" in kinds) == (len(prog.scope("E").sums) > 1)
+
+
+def test_relax_split_iter_permute_and_merge_keep_the_value():
+    prog = D.conv2d_expr(1, 2, 5, 5, 2, 5, 4, (1, 1), (2, 1), (1, 1))
+    t = rand_inputs(prog, 7)
+    ref = value(prog, t)
+    p = D.relax(prog, "E", "r", 6)
+    assert p is not None and np.array_equal(value(p, t), ref)
+    pc = D.relax(prog, "E", "c", 3)                    # c = 2 reads K's padding: adds 0
+    assert pc is not None and np.array_equal(value(pc, t), ref)
+    assert D.relax(prog, "E", "c", 2) is None          # not an extension
+    # r over [0, 3) of a 5-row kernel: r = 3 reads a real weight row, so no relaxing
+    e = prog.scope("E")
+    short = D.Program(prog.inputs, (("E", D.Scope(e.trav, (D.Iter("r", 0, 3),) + e.sums[1:],
+                                                   e.refs)),), "E")
+    assert D.relax(short, "E", "r", 4) is None
+    p = D.split_iter(p, "E", "r", 3, "a", "rr")
+    assert np.array_equal(value(p, t), ref)
+    p = D.split_summation(p, "E", ("rr", "s", "c"))
+    inner = [n for n, _ in p.scopes if n != "E"][0]
+    order = [i.name for i in p.scope(inner).trav][::-1]
+    q = D.permute(p, inner, order)
+    assert np.array_equal(value(q, t), ref)
+    # a pure re-indexing scope folds back into its reader
+    base = D.conv2d_expr(1, 1, 3, 3, 1, 1, 1)
+    x = D.Scope(base.scope("E").trav, (), (D.Ref("A", tuple(D.Aff.var(i.name) for i in
+                                                             base.scope("E").trav)),))
+    two = D.Program(base.inputs, (("E", D.Scope(base.scope("E").trav, (),
+                                                  (D.Ref("X", tuple(D.Aff.var(i.name) for i in
+                                                                    base.scope("E").trav)),))),
+                                  ("X", x)), "E")
+    merged = D.merge_traversal(two, "X")
+    assert merged is not None and len(merged.scopes) == 1
+    ti = rand_inputs(two, 8)
+    assert np.array_equal(value(merged, ti), value(two, ti))
+
+
+def test_fingerprint_ignores_names_and_summation_order_but_not_layout():
+    e = D.conv2d_expr(1, 2, 4, 4, 2, 3, 3, (1, 1), (1, 1), (1, 1))
+    s = e.scope("E")
+    ren = {"n": "q", "ho": "y", "wo": "x", "f": "o", "r": "u", "s": "v", "c": "z"}
+
+    def rename(sc):
+        return D.Scope(tuple(D.Iter(ren[i.name], i.lo, i.hi) for i in sc.trav),
+                       tuple(D.Iter(ren[i.name], i.lo, i.hi) for i in sc.sums),
+                       tuple(D.Ref(r.tensor, tuple(a.rename(ren) for a in r.idx))
+                             for r in sc.refs))
+    renamed = D.Program(e.inputs, (("E", rename(s)),), "E")
+    reordered = D.Program(e.inputs, (("E", D.Scope(s.trav, s.sums[::-1], s.refs[::-1])),), "E")
+    relaid = D.Program(e.inputs, (("E", D.Scope(s.trav[::-1], s.sums, s.refs)),), "E")
+    assert D.fingerprint(renamed) == D.fingerprint(e)
+    assert D.fingerprint(reordered) == D.fingerprint(e)
+    assert D.fingerprint(relaid) != D.fingerprint(e)          # traversal order = layout
+
+
+def test_fingerprint_pruning_cuts_the_search():
+    prog = D.conv2d_expr(1, 3, 5, 4, 2, 3, 3, (1, 1), (1, 1), (1, 1))
+    on, off = {}, {}
+    r1 = D.derive(prog, max_depth=4, stats=on)
+    r2 = D.derive(prog, max_depth=4, prune=False, stats=off, max_states=10 ** 6)
+    assert on["pruned"] > 0 and on["states"] < off["states"]
+    assert {D.fingerprint(d.prog) for d in r1} <= {D.fingerprint(d.prog) for d in r2}
+
+
+def test_conv3x3_derivation_is_the_papers_matmul_plus_offsetadd():
+    """The search reaches Matmul + OffsetAdd with the iterator mapping
+    t1, t2 -> m; r, s, f -> n; c -> k and the operand layouts of Eq. (3) and (4)."""
+    prog = D.conv2d_expr(1, 3, 6, 5, 4, 3, 3, (1, 1), (1, 1), (1, 1))
+    plan, dv = D.derive_conv(prog)
+    m = dv.matches[0]
+    assert m.op == "Matmul"
+    assert m.groups["m"][0] == "n" and len(m.groups["m"]) == 3      # n, t1, t2
+    assert m.groups["n"] == ["r", "s", "f"] and m.groups["k"] == ["c"]
+    inner = dv.prog.scope(m.scope)
+    a, w = inner.refs
+    assert a.tensor == "A" and [x.iters() for x in a.idx] == [(k,) for k in m.groups["m"]] + [("c",)]
+    assert w.tensor == "K" and [x.iters() for x in w.idx] == [("r",), ("s",), ("f",), ("c",)]
+    assert [s_[0] for s_ in dv.steps] == ["split", "subst", "subst", "tighten", "permute"]
+    assert (plan.M, plan.N, plan.K) == (1 * 6 * 5, 3 * 3 * 4, 3)
+
+
+CONV_GRID = [  # n, c, h, w, k, r, s, stride, pad, dil
+    (1, 2, 5, 4, 2, 3, 3, (1, 1), (1, 1), (1, 1)),
+    (2, 1, 6, 5, 2, 3, 2, (2, 1), (1, 0), (1, 2)),
+    (1, 2, 7, 7, 1, 3, 3, (1, 1), (2, 2), (2, 2)),
+    (1, 1, 5, 6, 2, 1, 1, (1, 1), (0, 0), (1, 1)),
+]
+CONVT_GRID = [  # n, c, h, w, k, r, s, stride, pad, dil, out_pad
+    (1, 2, 3, 3, 2, 4, 4, (2, 2), (1, 1), (1, 1), (0, 0)),
+    (1, 1, 3, 4, 2, 3, 2, (1, 1), (1, 0), (1, 1), (0, 0)),
+    (1, 2, 3, 4, 1, 3, 3, (3, 2), (1, 2), (2, 1), (1, 0)),
+]
+
+
+@pytest.mark.parametrize("gi", range(len(CONV_GRID)))
+def test_conv_plans_are_the_library_descriptors_and_the_definition(gi):
+    n, c, h, w, k, r, s, st, pd, dl = CONV_GRID[gi]
+    prog = D.conv2d_expr(n, c, h, w, k, r, s, st, pd, dl)
+    plan, dv = D.derive_conv(prog)
+    f = D.conv_desc_fields(plan, n, c, h, w, k, r, s)
+    d = ol.conv_desc((n, h, w, c), (r, s, k, c), st, pd, dl)
+    for key, v in f.items():
+        assert getattr(d, key) == v, key
+    t = rand_inputs(prog, 200 + gi)
+    ref = oracle.conv2d(t["A"].astype(np.float32), t["K"].astype(np.float32), st, pd, dl)
+    assert np.array_equal(value(dv.prog, t), ref)
+
+
+@pytest.mark.parametrize("gi", range(len(CONVT_GRID)))
+def test_convt_plans_are_the_selective_add_and_the_definition(gi):
+    n, c, h, w, k, r, s, st, pd, dl, op = CONVT_GRID[gi]
+    prog = D.conv_transpose2d_expr(n, c, h, w, k, r, s, st, pd, dl, op)
+    plan, dv = D.derive_conv(prog, transposed=True)
+    assert plan.transposed and (plan.stride, plan.pad, plan.dil) == (st, pd, dl)
+    assert (plan.M, plan.N, plan.K) == (n * h * w, r * s * k, c)
+    t = rand_inputs(prog, 300 + gi)
+    ref = oracle.conv_transpose2d(t["X"].astype(np.float32), t["K"].astype(np.float32), st,
+                                  pd, dl, op)
+    assert np.array_equal(value(dv.prog, t), ref)
+    # the eOperator keeps one divisibility guard per strided axis
+    eop = dv.prog.scope("E")
+    assert sum(1 for g in eop.guards if g.mod) == sum(1 for x in st if x > 1)
+
+
+@pytest.mark.parametrize("b,l,d,w,dil", [(1, 9, 3, 2, 2), (2, 11, 2, 1, 3), (1, 6, 2, 3, 1)])
+def test_band_plan_is_the_residue_subsequences(b, l, d, w, dil):
+    """The dilated G2BMM matches the G2BMM pattern with dilation D; its residues are
+    the strided views the band kernel walks (length ceil((l - rho) / D)), each a band
+    of dilation 1, and evaluating them reproduces the oracle's scores."""
+    plan, m0, m1 = D.derive_band(b, l, d, w, dil)
+    assert m0.detail["dilation"] == dil and m0.detail["w"] == w
+    assert plan.residues == [(rho, dil, (l - rho + dil - 1) // dil) for rho in range(dil)
+                             if l - rho > 0]
+    prog = D.g2bmm_expr(b, l, d, w, dil)
+    t = rand_inputs(prog, 400)
+    s_full = value(prog, t)
+    s_ref, _, _ = oracle.band(t["Q"].astype(np.float32), t["K"].astype(np.float32),
+                              np.zeros_like(t["Q"], dtype=np.float32), w, dil)
+    assert np.array_equal(s_full, s_ref)
+    for rho, stp, n in plan.residues:
+        sub = D._residue_band(b, l, d, w, dil, rho, n)
+        tr = {"QR": t["Q"][:, rho::stp], "KR": t["K"][:, rho::stp]}
+        assert np.array_equal(value(sub, tr), s_full[:, rho::stp])
+
+
+@pytest.mark.parametrize("args", [(1, 2, 7, 6, 2, 5, 5, (2, 2)), (1, 2, 6, 7, 2, 4, 2, (1, 0)),
+                                  (1, 1, 8, 5, 1, 7, 3, (3, 1))])
+def test_split3x3_plan_is_the_librarys_and_the_definition(args):
+    """The rewrite reached by relaxing, splitting and substituting: a 3x3 Conv stage
+    with ceil(R/3)*ceil(S/3)*K channels padded by p + er, and block offsets er + 3a --
+    the geometry derived_conv2d's OLLIE_CONV_SPLIT_3X3 path uses."""
+    n, c, h, w, k, r, s, pad = args
+    plan, p = D.derive_split3x3(*args)
+    nbr, nbs = -(-r // 3), -(-s // 3)
+    er, es = 3 * nbr - r, 3 * nbs - s
+    assert (plan.nbr, plan.nbs) == (nbr, nbs)
+    assert plan.pad3 == (pad[0] + er, pad[1] + es) == plan.conv.detail["pad"]
+    assert plan.offsets == [(er + 3 * a, es + 3 * b) for a in range(nbr) for b in range(nbs)]
+    assert plan.conv.detail["K"] == nbr * nbs * k
+    t = rand_inputs(D.conv2d_expr(n, c, h, w, k, r, s, (1, 1), pad), 500)
+    ref = oracle.conv2d(t["A"].astype(np.float32), t["K"].astype(np.float32), 1, pad, 1)
+    assert np.array_equal(value(p, t), ref)
