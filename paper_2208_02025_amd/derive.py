@@ -59,6 +59,8 @@ class Aff:
     def __add__(self, o) -> "Aff":
         if isinstance(o, int):
             return Aff(self.terms, self.const + o)
+        if isinstance(o, Quot):
+            return o + self
         d = dict(self.terms)
         for k, v in o.terms:
             d[k] = d.get(k, 0) + v
@@ -475,6 +477,34 @@ class Quot(Aff):
     def iters(self):
         return self.num.iters()
 
+    # Exact wherever a guard makes num divisible by den; any other combination would
+    # lose the division, so it raises and the rule that asked declines.
+    def __add__(self, o) -> "Quot":
+        if isinstance(o, int):
+            return Quot(self.num, self.den, self.add + o)
+        if isinstance(o, Aff) and not isinstance(o, Quot) and not o.terms:
+            return Quot(self.num, self.den, self.add + o.const)
+        raise TypeError("a quotient index combines only with constants")
+
+    def __sub__(self, o) -> "Quot":
+        if isinstance(o, int):
+            return self + (-o)
+        raise TypeError("a quotient index combines only with constants")
+
+    def __mul__(self, c: int) -> "Quot":
+        return Quot(self.num * c, self.den, self.add * c)
+
+    def subs(self, name: str, e: Aff) -> "Quot":
+        if isinstance(e, Quot):
+            raise TypeError("nested quotient")
+        return Quot(self.num.subs(name, e), self.den, self.add)
+
+    def rename(self, m: Dict[str, str]) -> "Quot":
+        return Quot(self.num.rename(m), self.den, self.add)
+
+    def bounds(self, rng):
+        raise TypeError("no box for a quotient index")
+
     def __str__(self):
         return "(%s)/%d%s" % (self.num, self.den, "+%d" % self.add if self.add else "")
 
@@ -665,23 +695,36 @@ MATCHERS = {"Matmul": match_matmul, "Conv": match_conv, "G2BMM": match_g2bmm}
 
 # ------------------------------------------------------------ hybrid derivation
 
+def _try(rule, *args):
+    """A rule application, or None where the rule would have to combine a quotient
+    index non-exactly (it declines instead of miscomputing)."""
+    try:
+        return rule(*args)
+    except TypeError:
+        return None
+
+
 def _moves(prog: Program):
     """Every rule application the explorative stage tries on a program."""
+    return _moves_all(prog)
+
+
+def _moves_all(prog: Program):
     for name, s in prog.scopes:
         sn = [i.name for i in s.sums]
         for k in range(1, len(sn)):
             for inner in itertools.combinations(sn, k):
-                p = split_summation(prog, name, inner)
+                p = _try(split_summation, prog, name, inner)
                 if p is not None:
                     yield ("split", name, inner), p
-        p = tighten(prog, name)
+        p = _try(tighten, prog, name)
         if p is not None:
             yield ("tighten", name), p
-        p = merge_traversal(prog, name)
+        p = _try(merge_traversal, prog, name)
         if p is not None:
             yield ("merge", name), p
         for x in sorted({k for g in s.guards if not g.mod for k in g.aff.iters()}):
-            p = eliminate_guard(prog, name, x)
+            p = _try(eliminate_guard, prog, name, x)
             if p is not None:
                 yield ("eliminate", name, x), p
         # substitution candidates: a multi-iterator index expression over this
@@ -698,7 +741,7 @@ def _moves(prog: Program):
                 taken = set(s.ranges())
                 fresh = next("t%d" % k for k in itertools.count() if "t%d" % k not in taken)
                 for old, c in a.terms:
-                    p = substitute(prog, name, old, a, fresh)
+                    p = _try(substitute, prog, name, old, a, fresh)
                     if p is not None:
                         yield ("subst", name, old, str(a)), p
 

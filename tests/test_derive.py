@@ -213,3 +213,27 @@ def test_split3x3_plan_is_the_librarys_and_the_definition(args):
     t = rand_inputs(D.conv2d_expr(n, c, h, w, k, r, s, (1, 1), pad), 500)
     ref = oracle.conv2d(t["A"].astype(np.float32), t["K"].astype(np.float32), 1, pad, 1)
     assert np.array_equal(value(p, t), ref)
+
+
+def test_quotient_index_arithmetic_is_exact_or_declines():
+    """(num / den) indices (the selective add) combine exactly with constants, scaling
+    and substitution inside num; a sum with another iterator cannot stay a quotient,
+    so it raises and the search's rule application declines instead."""
+    q = D.Quot(D.Aff.of({"ho": 1, "r": -1}, 1), 2)
+    env = {"ho": 5, "r": 2, "x": 3}
+    assert q.eval(env) == 2
+    assert (q + 3).eval(env) == 5
+    assert (q * 2).eval(env) == 4
+    assert q.subs("ho", D.Aff.of({"x": 2}, 1)).eval(env) == (2 * 3 + 1 - 2 + 1) // 2
+    with pytest.raises(TypeError):
+        q + D.Aff.var("x")
+    with pytest.raises(TypeError):
+        D.Aff.var("x") + q
+    # the derived transposed program has quotient indices; further search steps from it
+    # never miscompute (every move keeps the value)
+    prog = D.conv_transpose2d_expr(1, 1, 3, 3, 1, 3, 3, (2, 2), (1, 1), (1, 1), (1, 1))
+    plan, dv = D.derive_conv(prog, transposed=True)
+    t = rand_inputs(prog, 600)
+    ref = value(prog, t)
+    for mv, q2 in D._moves(dv.prog):
+        assert np.array_equal(value(q2, t), ref), mv
