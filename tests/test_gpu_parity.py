@@ -749,27 +749,37 @@ def test_hip_graph_replays_match_eager():
     o2 = torch.empty((16, 14, 14, 256), device=DEV)
     o4 = torch.empty((1, 96, 128, 512), device=DEV)
     ob = torch.empty((4, 777, 64), device=DEV)
+    # the 3x3 split form: weight split, 3x3 stage and block OffsetAdd in one call
+    x5 = synth.random_tensor((2, 21, 19, 64), 19010, "bf16", dist="normal").to(DEV)
+    w5 = synth.random_tensor((5, 5, 24, 64), 19011, "bf16", dist="normal").to(DEV)
+    desc5 = ol.conv_desc(tuple(x5.shape), tuple(w5.shape), 1, 2, 1, 0, x5.dtype, torch.float32)
+    ws5 = torch.empty(ol.conv_workspace_bytes(desc5, False, ol.CONV_SPLIT_3X3 | ol.FUSE_EPILOGUE),
+                      dtype=torch.uint8, device=DEV)
+    o5 = torch.empty((2, 21, 19, 24), device=DEV)
 
     def calls():
         ol.derived_conv2d(x2, w2, 1, 1, out=o2, ws=ws2)
         ol.derived_dilated_conv2d(x4, w4, 1, 2, 2, out=o4, fuse=True)
         ol.banded_bmm(q, k, v, 40, 3, 0.125, out=ob)
+        ol.derived_conv2d(x5, w5, 1, 2, out=o5, ws=ws5, fuse=True, split3x3=True)
 
+    outs = (o2, o4, ob, o5)
     calls()
     torch.cuda.synchronize()
-    ref = [o2.clone(), o4.clone(), ob.clone()]
+    ref = [t.clone() for t in outs]
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         calls()
     for i in range(4):
-        for t in (o2, o4, ob):
+        for t in outs:
             t.fill_(float("nan"))
+        ws5.fill_(0xff)                                  # stale workspace between replays
         junk = torch.randn(1 << 20, device=DEV) * i      # unrelated eager work
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
         assert float(junk.abs().sum()) >= 0
-        for got, exp in zip((o2, o4, ob), ref):
+        for got, exp in zip(outs, ref):
             assert torch.equal(got, exp), f"replay {i} differs from the eager result"
 
 
