@@ -141,7 +141,9 @@ int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, 
 size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags);
 
 /* Bytes of workspace banded_bmm needs: 0 for the fused path; with OLLIE_BAND_STAGED,
- * S [b][l][2w+1] fp32 followed (at a 256-byte aligned offset) by P [b][l][2w+1] bf16. */
+ * S [b][l][2w+1] fp32 followed (at a 256-byte aligned offset) by P [b][l][2w+1] bf16.
+ * Returns 0 for a descriptor banded_bmm rejects (invalid geometry, or a staged band
+ * wider than 1024 entries). */
 size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags);
 
 /* Message for the last failure on this thread ("" if none); valid until the next

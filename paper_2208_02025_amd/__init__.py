@@ -2,7 +2,8 @@
 
 Argument marshalling only: every step of every operator runs in the library's HIP
 kernels.  torch provides device memory and the current HIP stream.  There is no CPU
-fallback: if libollie.so is missing or the tensors are not on a GPU, calls raise.
+fallback: a missing libollie.so is built from csrc/ with hipcc on first use (and the
+call raises if that fails), and tensors that are not on a GPU raise.
 
 Layouts (contiguous):
   x   [n][h][w][c] (NHWC)          wt  [r][s][k][c]  (torch conv2d weight .permute(2,3,0,1),

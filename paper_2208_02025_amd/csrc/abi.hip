@@ -368,6 +368,7 @@ size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, u
 size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags) {
     if (check_band(desc)) return 0;
     if (!(flags & OLLIE_BAND_STAGED)) return 0;
+    if (2 * desc->w + 1 > kSoftmaxMaxBand) return 0;   // banded_bmm rejects this band
     return band_p_offset(desc) + band_p_bytes(desc);
 }
 

@@ -152,6 +152,12 @@ def test_band_workspace_bytes(lib):
     s_bytes = 96 * 4096 * 513 * 4
     p_off = (s_bytes + 255) // 256 * 256
     assert ol.band_workspace_bytes(d, ol.BAND_STAGED) == p_off + 96 * 4096 * 513 * 2
+    # the staged softmax holds at most 1024 band entries per row: wider bands, which
+    # banded_bmm rejects, and invalid descriptors need no workspace size
+    assert ol.band_workspace_bytes(band(w=511), ol.BAND_STAGED) > 0
+    assert ol.band_workspace_bytes(band(w=512), ol.BAND_STAGED) == 0
+    assert ol.band_workspace_bytes(band(w=1 << 29), ol.BAND_STAGED) == 0
+    assert ol.band_workspace_bytes(band(b=0), ol.BAND_STAGED) == 0
 
 
 def test_gemm_error_paths(lib):
