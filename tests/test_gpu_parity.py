@@ -468,6 +468,7 @@ BAND_SMALL = [  # (b, l, w, dil)
     (2, 64, 0, 1),        # window of one
     (1, 1, 3, 1),         # single row
     (1, 515, 64, 4),
+    (2, 3, 2, 5),         # dilation above the length: residues 3 and 4 are empty
 ]
 
 

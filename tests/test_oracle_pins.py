@@ -344,6 +344,24 @@ def test_band_mask_mode_full_window_is_softmax_attention():
                                    rtol=0, atol=1e-14)
 
 
+def test_band_lone_entry_rows_return_v():
+    """With the dilation at or above the sequence length every key t = i + (j-w)*D other
+    than t = i falls outside [0, L): in mask mode each row's softmax has the single entry
+    j = w, so P is one-hot and O equals V exactly; in zero mode the 2w out-of-range
+    entries score 0 and O = e^s V / (e^s + 2w) with s = scale * q.k."""
+    b, l, d, w, dil = 2, 3, 5, 2, 5
+    q, k, v = _band_inputs(b, l, d, 1250)
+    s, p, o = oracle.band(q, k, v, w, dil, scale=0.3, mask=True)
+    onehot = np.zeros(2 * w + 1)
+    onehot[w] = 1.0
+    np.testing.assert_array_equal(p, np.broadcast_to(onehot, p.shape))
+    np.testing.assert_array_equal(o, v)
+    _, _, oz = oracle.band(q, k, v, w, dil, scale=0.3, mask=False)
+    q64, k64, v64 = (a.astype(np.float64) for a in (q, k, v))
+    es = np.exp(0.3 * np.einsum("bid,bid->bi", q64, k64))[..., None]
+    np.testing.assert_allclose(oz, es * v64 / (es + 2 * w), rtol=1e-13, atol=0)
+
+
 @pytest.mark.parametrize("ci", range(len(BAND_CASES)))
 def test_band_zero_mode_is_attention_over_zero_padded_keys(ci):
     """Zero mode = softmax attention in which every out-of-range key and value is an
