@@ -179,20 +179,25 @@ __device__ __forceinline__ int n_key_blocks(const BandGeom& g) {
 }
 
 // --------------------------------------------------------------------- G2BMM
+// Each wave owns 16 queries.  A block's 16 x 64 scores go through LDS so that they leave
+// row by row: for one query the block's 64 keys are 64 consecutive band entries of its
+// S row (j = key - query + w), written by the 64 lanes as one contiguous segment.
+constexpr int kPatchLd = kT + 4;   // fp32 row stride of a wave's score patch in LDS
 __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
                                                         const bf16_t* __restrict__ Q,
                                                         const bf16_t* __restrict__ K,
                                                         float* __restrict__ S) {
     __shared__ u32x4 lk[kT * 8];
+    __shared__ __attribute__((aligned(16))) float ls[4][16 * kPatchLd];
     Tile t;
     if (!tile_of(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
-    const int q = t.q0 + wv * 16 + (lane & 15);
+    const int qw = t.q0 + wv * 16;                  // the wave's first query
     const int w = (int)g.w, nb = 2 * w + 1;
     bf16x8 qf[2];
-    load_q_frags(g, t, Q, q, qf);
+    load_q_frags(g, t, Q, qw + (lane & 15), qf);
     const int nblk = n_key_blocks(g);
-    float* srow = S + (q < t.lr ? row_index(g, t, q) : 0) * nb;
+    float* patch = ls[wv];
     KVRegs r;
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
@@ -202,14 +207,18 @@ __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
         __syncthreads();
         f32x4 s[4];
         score_block(lk, qf, s);
-        if (q >= t.lr) continue;
 #pragma unroll
-        for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int j = t0 + ft * 16 + 4 * grp + v - q + w;
-                if (j >= 0 && j < nb) srow[j] = g.scale * s[ft][v];
-            }
+        for (int ft = 0; ft < 4; ++ft)   // query lane%16, keys 16ft + 4grp .. +3
+            *reinterpret_cast<f32x4*>(patch + (lane & 15) * kPatchLd + ft * 16 + 4 * grp) =
+                s[ft] * g.scale;
+        __syncthreads();
+#pragma unroll 4
+        for (int rr = 0; rr < 16; ++rr) {
+            const int qq = qw + rr;
+            const int j = t0 + lane - qq + w;    // lane = key offset in the block
+            if (qq < t.lr && j >= 0 && j < nb)
+                S[row_index(g, t, qq) * nb + j] = patch[rr * kPatchLd + lane];
+        }
     }
 }
 
@@ -261,19 +270,25 @@ __global__ __launch_bounds__(256) void band_softmax_kernel(BandGeom g, const flo
 }
 
 // ---------------------------------------------------------------------- GBMM
+// The probabilities of a block arrive the same way the scores leave the G2BMM: row by
+// row, the 64 lanes reading one query's 64 consecutive band entries, through a per-wave
+// LDS patch from which each lane takes its MFMA operand.
+constexpr int kPLd = kT + 8;   // bf16 row stride of a wave's probability patch in LDS
 template <typename OT>
 __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
                                                        const bf16_t* __restrict__ P,
                                                        const bf16_t* __restrict__ V,
                                                        OT* __restrict__ O) {
     __shared__ __attribute__((aligned(16))) bf16_t lv[kT * kVLd];
+    __shared__ __attribute__((aligned(16))) bf16_t lp[4][16 * kPLd];
     Tile t;
     if (!tile_of(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
-    const int q = t.q0 + wv * 16 + (lane & 15);
+    const int qw = t.q0 + wv * 16;
+    const int q = qw + (lane & 15);
     const int w = (int)g.w, nb = 2 * w + 1;
-    const bf16_t* prow = P + (q < t.lr ? row_index(g, t, q) : 0) * nb;
     const int nblk = n_key_blocks(g);
+    bf16_t* patch = lp[wv];
     f32x4 o[4];
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
@@ -281,17 +296,25 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
         gload_block<false, true>(g, t, nullptr, V, t0, r);
+#pragma unroll 4
+        for (int rr = 0; rr < 16; ++rr) {
+            const int qq = qw + rr;
+            const int j = t0 + lane - qq + w;
+            bf16_t val = 0;
+            if (qq < t.lr && j >= 0 && j < nb) val = P[row_index(g, t, qq) * nb + j];
+            patch[rr * kPLd + lane] = val;
+        }
         __syncthreads();
         lstore_block<false, true>(r, nullptr, lv);
         __syncthreads();
         f32x4 p[4];
 #pragma unroll
-        for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int j = t0 + ft * 16 + 4 * grp + v - q + w;
-                p[ft][v] = (q < t.lr && j >= 0 && j < nb) ? bf2f(prow[j]) : 0.f;
-            }
+        for (int ft = 0; ft < 4; ++ft) {   // keys 16ft + 4grp .. +3 of query lane%16
+            const uint2 u = *reinterpret_cast<const uint2*>(patch + (lane & 15) * kPLd +
+                                                            ft * 16 + 4 * grp);
+            p[ft] = (f32x4){__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                            __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+        }
         pv_block(lv, p, o);
     }
     if (q >= t.lr) return;
