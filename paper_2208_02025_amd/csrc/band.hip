@@ -199,12 +199,14 @@ __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
     const int nblk = n_key_blocks(g);
     float* patch = ls[wv];
     KVRegs r;
+    gload_block<true, false>(g, t, K, nullptr, t.q0 - w, r);
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
-        gload_block<true, false>(g, t, K, nullptr, t0, r);
         __syncthreads();
         lstore_block<true, false>(r, lk, nullptr);
         __syncthreads();
+        // the next key block's loads overlap this block's scores and row stores
+        if (kb + 1 < nblk) gload_block<true, false>(g, t, K, nullptr, t0 + kT, r);
         f32x4 s[4];
         score_block(lk, qf, s);
 #pragma unroll
@@ -293,9 +295,9 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
     KVRegs r;
+    gload_block<false, true>(g, t, nullptr, V, t.q0 - w, r);
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
-        gload_block<false, true>(g, t, nullptr, V, t0, r);
 #pragma unroll 4
         for (int rr = 0; rr < 16; ++rr) {
             const int qq = qw + rr;
@@ -307,6 +309,8 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
         __syncthreads();
         lstore_block<false, true>(r, nullptr, lv);
         __syncthreads();
+        // the next value block's loads overlap this block's products
+        if (kb + 1 < nblk) gload_block<false, true>(g, t, nullptr, V, t0 + kT, r);
         f32x4 p[4];
 #pragma unroll
         for (int ft = 0; ft < 4; ++ft) {   // keys 16ft + 4grp .. +3 of query lane%16
