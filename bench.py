@@ -12,8 +12,9 @@ both variants are timed and reported.
 `value` is the step's algorithmic TFLOP/s (all GEMM-stage and band contractions over
 the step time).  Per workload it also reports the GEMM stage in TFLOP/s and % of the
 bf16 MFMA peak (and, since its fp32 Y makes it HBM-bound on these shapes, its HBM
-GB/s and % of the roofline that binds it), the eOperator stage in GB/s and % of the
-HBM peak, and the fused kernel in TFLOP/s, each measured two ways:
+GB/s and % of the roofline that binds it; the same stage with a bf16 Y appears warm as
+gemm_ybf16_*), the eOperator stage in GB/s and % of the HBM peak, and the fused kernel
+in TFLOP/s, each measured two ways:
   warm     HIP events around a HIP graph of back-to-back launches of that kernel (host
            launch gaps do not count), on the stream it runs on;
   cold     ("cold" block) the median of single launches, each bracketed by HIP events
@@ -318,6 +319,10 @@ def main():
         kw_f = {k_: v_ for k_, v_ in op["kw"].items() if k_ != "residues"}
         f_fn = lambda: op["entry"](op["x"], op["wt"], **dict(kw_f, ws=None, fuse=True))
         g_ms = time_kernel(g_fn, reps)
+        # the same GEMM stage with its scope Y held in bf16 (OLLIE_Y_BF16): half of Y's
+        # bytes; a variant reported beside the fp32 default, never the headline
+        yb = op["ws"][:op["m"] * op["nc"] * 2].view(torch.bfloat16).view(op["m"], op["nc"])
+        gb_ms = time_kernel(lambda: ol.gemm_nt(a, b, y_dtype=torch.bfloat16, out=yb), reps)
         e_ms = time_kernel(e_fn, reps)
         f_ms = time_kernel(f_fn, reps)
         g_cold = time_kernel_cold(g_fn, reps_cold)
@@ -348,6 +353,9 @@ def main():
             "gemm_hbm_gbs": round(g_gb, 1), "gemm_pct_hbm_peak": round(100 * g_gb / PEAK_HBM_GBS, 2),
             "gemm_bound": g_bound,
             "gemm_pct_roofline": round(100 * max(t_mfma, t_hbm) / (g_ms * 1e-3), 2),
+            "gemm_ybf16_ms": round(gb_ms, 5),
+            "gemm_ybf16_tflops": round(op["flops"] / (gb_ms * 1e-3) / 1e12, 2),
+            "gemm_ybf16_pct_mfma_peak": round(100 * t_mfma / (gb_ms * 1e-3), 2),
             "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
             "eop_pct_hbm_peak": round(100 * e_gb / PEAK_HBM_GBS, 2),
             "fused_ms": round(f_ms, 5), "fused_tflops": round(f_tf, 2),
