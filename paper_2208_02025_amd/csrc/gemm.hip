@@ -27,6 +27,8 @@
 // consecutive output columns n of one row m.
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace ollie {
@@ -115,6 +117,35 @@ __device__ __forceinline__ void store_tile_rows(YT* __restrict__ Y, const f32x4 
             }
         }
         __syncthreads();
+        if constexpr (std::is_same<YT, bf16_t>::value && (RP * CH / 2) % NT == 0) {
+            // bf16 rows: two chunks (8 values) per lane and one 16-byte store
+            const bool vec8_ok = (N & 7) == 0;
+#pragma unroll
+            for (int it = 0; it < RP * CH / 2 / NT; ++it) {
+                const int e = it * NT + tid;
+                const int r = e / (CH / 2), c = 2 * (e % (CH / 2));
+                const f32x4 v0 = t[r * CH + (c ^ (r & 15))];
+                const f32x4 v1 = t[r * CH + ((c + 1) ^ (r & 15))];
+                const int64_t m = m0 + p * RP + r, n = n0 + 4 * c;
+                if (m >= M) continue;
+                YT* dst = Y + m * N + n;
+                if (vec8_ok && n + 7 < N) {
+                    u32x4 u;
+                    u[0] = (uint32_t)f2bf(v0[0]) | ((uint32_t)f2bf(v0[1]) << 16);
+                    u[1] = (uint32_t)f2bf(v0[2]) | ((uint32_t)f2bf(v0[3]) << 16);
+                    u[2] = (uint32_t)f2bf(v1[0]) | ((uint32_t)f2bf(v1[1]) << 16);
+                    u[3] = (uint32_t)f2bf(v1[2]) | ((uint32_t)f2bf(v1[3]) << 16);
+                    *reinterpret_cast<u32x4*>(dst) = u;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (n + q < N) Out<YT>::put(dst + q, v0[q]);
+                        if (n + 4 + q < N) Out<YT>::put(dst + 4 + q, v1[q]);
+                    }
+                }
+            }
+            continue;
+        }
 #pragma unroll
         for (int it = 0; it < RP * CH / NT; ++it) {
             const int e = it * NT + tid;
