@@ -28,9 +28,9 @@
  * last failure on the calling thread.
  *
  * Common buffer rules: tensors are dense and row-major in the layouts stated below;
- * pointers must be 16-byte aligned (else OLLIE_EALIGN); outputs must not alias
- * inputs or the workspace (one stated exception: a fused residual, see
- * ollie_conv_epilogue).
+ * pointers must be 16-byte aligned (else OLLIE_EALIGN); outputs must not overlap
+ * inputs or the workspace (else OLLIE_EINVAL; one stated exception: a fused residual
+ * that is the output buffer itself, see ollie_conv_epilogue).
  */
 #ifndef OLLIE_H
 #define OLLIE_H
@@ -63,6 +63,20 @@ typedef enum {
 #define OLLIE_BAND_MASK_INVALID (1u << 3)  /* band: keys outside [0,l) are left out of the softmax */
 #define OLLIE_DILATED_RESIDUES  (1u << 4)  /* dilated conv: as non-dilated convs over residue sub-images */
 #define OLLIE_CONV_SPLIT_3X3    (1u << 5)  /* conv: as a 3x3 convolution over kernel blocks + OffsetAdd */
+
+/* Tile-configuration overrides, for tuning sweeps and tests (these bits zero = the
+ * library's automatic choice, which is what every other caller should use).  They
+ * change which kernel instance evaluates the expression, never what it computes.
+ *   OLLIE_FUSED_TILE(n), n in 0..14: tile shape of the fused GEMM + eOperator kernel
+ *     (conv entry points; ignored when the call takes the two-stage path).
+ *   OLLIE_GEMM_TILE(n), n in 0..4: tile shape of the GEMM stage kernel (conv entry
+ *     points on the two-stage path; ignored on the fused path).
+ *   OLLIE_BAND_SHAPE(n), n in 0..2: wave shape of the fused band kernel (banded_bmm
+ *     without OLLIE_BAND_STAGED).
+ * An n outside its range gives OLLIE_EINVAL. */
+#define OLLIE_FUSED_TILE(n)     ((uint32_t)(((n) + 1) & 0xff) << 16)
+#define OLLIE_GEMM_TILE(n)      ((uint32_t)(((n) + 1) & 0xf) << 24)
+#define OLLIE_BAND_SHAPE(n)     ((uint32_t)(((n) + 1) & 0xff) << 16)
 
 /* Geometry of a convolution-family operator.
  *   X   [n][h][w][c]   input (NHWC).  As a GEMM operand it is A'[m][c] with
@@ -126,14 +140,17 @@ typedef struct {
 /* ------------------------------------------------------------------ helpers */
 
 /* Output extent of the operator (transposed = 0: conv2d / dilated conv2d,
- * 1: conv_transpose2d):
+ * 1: conv_transpose2d), the traversal range of the output scope of the convolution
+ * expression (section 3, section 4.2 with zero padding; the transposed operator as
+ * the adjoint of the convolution, section 6.3):
  *   forward    ho = floor((h + 2*pad_h - dil_h*(r-1) - 1) / stride_h) + 1
  *   transposed ho = (h-1)*stride_h - 2*pad_h + dil_h*(r-1) + out_pad_h + 1
  * and likewise for wo.  Returns OLLIE_EINVAL on invalid geometry or an empty output. */
 int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, int64_t* wo);
 
 /* Bytes of workspace that derived_conv2d / derived_dilated_conv2d /
- * derived_conv_transpose2d need: the instantiated scope Y [n*h*w][r*s*k] in fp32
+ * derived_conv_transpose2d need: the instantiated scope Y [n*h*w][r*s*k] of the
+ * matched Matmul (section 4.3.1, the scope instantiation of Eq. (3) and (4)) in fp32
  * (or bf16 with OLLIE_Y_BF16); 0 when OLLIE_FUSE_EPILOGUE is set and the fused kernel
  * covers the shape.  With OLLIE_CONV_SPLIT_3X3 (derived_conv2d): the split weights,
  * the 3x3 stage Z and that stage's own workspace (see derived_conv2d).  Returns 0 for
@@ -141,16 +158,19 @@ int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, 
 size_t ollie_conv_workspace_bytes(const ollie_conv_desc* desc, int transposed, uint32_t flags);
 
 /* Bytes of workspace banded_bmm needs: 0 for the fused path; with OLLIE_BAND_STAGED,
- * S [b][l][2w+1] fp32 followed (at a 256-byte aligned offset) by P [b][l][2w+1] bf16.
+ * the G2BMM output scope (Table 2: iterators b, i in every tensor, the band offset j
+ * in weight and output) S [b][l][2w+1] fp32 followed (at a 256-byte aligned offset) by P [b][l][2w+1] bf16.
  * Returns 0 for a descriptor banded_bmm rejects (invalid geometry, or a staged band
  * wider than 1024 entries). */
 size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags);
 
 /* Message for the last failure on this thread ("" if none); valid until the next
- * library call on this thread. */
+ * library call on this thread.  (Error reporting of the library; no passage of the
+ * paper defines it.) */
 const char* ollie_last_error(void);
 
-/* Library version string. */
+/* Library version string, e.g. "ollie-mi355x 0.2.0 (gfx950)".  (Not defined by the
+ * paper.) */
 const char* ollie_version(void);
 
 /* ------------------------------------------------------------- entry points */
@@ -169,8 +189,11 @@ const char* ollie_version(void);
  * OLLIE_FUSE_EPILOGUE evaluates the expression obtained by fusing the GEMM scope into
  * the eOperator (expression fusion, section 4.1): one contraction over (tap, c) per
  * output element, so Y is never formed and ws may be NULL.  It covers bf16 inputs with
- * c % 64 == 0, at most 64 taps and, for the transposed operator, at most 16 stride
- * residue classes; other shapes take the two-stage path, which needs the workspace.
+ * c % 64 == 0, r <= 64 and s <= 64 and at most 16 output residue classes (the
+ * transposed operator has stride_h*stride_w classes, the residue form dil_h*dil_w, the
+ * plain convolution one); other shapes take the two-stage path, which needs the
+ * workspace.  ollie_conv_workspace_bytes returning 0 for these flags is the test for
+ * the fused path.
  * Summation order differs from the two-stage path, so fp32 results agree to rounding
  * (integer-valued inputs agree exactly).
  *
@@ -224,19 +247,24 @@ int derived_conv_transpose2d(const ollie_conv_desc* desc, const void* x, const v
                              void* stream);
 
 /* The three operators above with an element-wise tail (ollie_conv_epilogue) fused
- * into their last kernel, for both the two-stage and the fused path.  epi == NULL is
- * the plain operator.  Extra checks: relu not in {0, 1} or a bias/residual pointer
- * that is not 16-byte aligned -> OLLIE_EINVAL / OLLIE_EALIGN; an unknown
- * bias_dtype/residual_dtype of a non-NULL tensor -> OLLIE_EDTYPE. */
-int derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
-                      void* ws, size_t ws_bytes, uint32_t flags,
-                      const ollie_conv_epilogue* epi, void* stream);
-int derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
-                              void* out, void* ws, size_t ws_bytes, uint32_t flags,
-                              const ollie_conv_epilogue* epi, void* stream);
-int derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
-                                void* out, void* ws, size_t ws_bytes, uint32_t flags,
-                                const ollie_conv_epilogue* epi, void* stream);
+ * into their last kernel, for both the two-stage and the fused path: the fusion of
+ * the eOperator with the element-wise operators after it (section 6.3, and the
+ * expression fusion of section 5.4).  epi == NULL is the plain operator.  Extra
+ * checks: relu not in {0, 1} -> OLLIE_EINVAL; a bias/residual pointer that is not
+ * 16-byte aligned -> OLLIE_EALIGN; an unknown bias_dtype/residual_dtype of a non-NULL
+ * tensor -> OLLIE_EDTYPE; a bias overlapping out, or a residual overlapping out
+ * other than exactly (same pointer) -> OLLIE_EINVAL. */
+int ollie_derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+                            void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                            const ollie_conv_epilogue* epi, void* stream);
+int ollie_derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x,
+                                    const void* wt, void* out, void* ws, size_t ws_bytes,
+                                    uint32_t flags, const ollie_conv_epilogue* epi,
+                                    void* stream);
+int ollie_derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x,
+                                      const void* wt, void* out, void* ws, size_t ws_bytes,
+                                      uint32_t flags, const ollie_conv_epilogue* epi,
+                                      void* stream);
 
 /* Banded dilated batched matmul with row softmax (Longformer-style sliding window):
  *   S[b][i][j] = scale * sum_e Q[b][i][e] * K0[b][t][e],  t = i + (j-w)*dilation
@@ -256,20 +284,37 @@ int banded_bmm(const ollie_band_desc* desc, const void* q, const void* k, const 
 
 /* ------------------------------------------------- stage entry points (same kernels) */
 
-/* GEMM stage alone: Y[m][n] = sum_kk A[m][kk] * B[n][kk] (A [m][k], B [n][k], Y [m][n]).
- * in_dtype F32 or BF16 (A and B); y_dtype F32 or BF16.  BF16 needs k % 8 == 0. */
+/* GEMM stage alone, the matched Matmul of the derived convolution forms (section 4.3.1;
+ * operand layouts of Eq. (3) and Eq. (4)):
+ *   Y[m][n] = sum_kk A[m][kk] * B[n][kk]   (A [m][k], B [n][k], Y [m][n], row-major).
+ * in_dtype F32 or BF16 (A and B); y_dtype F32 or BF16 (bf16 Y rounds the fp32 sum to
+ * nearest even).  BF16 needs k % 8 == 0 (else OLLIE_EALIGN).  y must not overlap a or b
+ * (OLLIE_EINVAL). */
 int ollie_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
                   int32_t in_dtype, int32_t y_dtype, void* stream);
 
-/* eOperator alone: y is the scope Y [n*h*w][r*s*k] in y_dtype; out as in the
- * descriptor.  transposed = 0: (dilated) OffsetAdd; 1: the transposed selective add. */
-int ollie_eop_gather(const ollie_conv_desc* desc, int transposed, const void* y,
-                     int32_t y_dtype, void* out, void* stream);
+/* OffsetAdd eOperator alone (section 2; taps spaced by the dilation, out-of-image taps
+ * never read, section 4.2 boundary tightening): y is the scope Y [n*h*w][r*s*k] in
+ * y_dtype, out [n][ho][wo][k] in desc->out_dtype,
+ *   out[n][ho][wo][k] = sum_{r,s} [0 <= hi < h][0 <= wi < w] Y[(n*h+hi)*w+wi][(r*S+s)*K+k]
+ *   hi = ho*stride_h - pad_h + r*dil_h, wi = wo*stride_w - pad_w + s*dil_w.
+ * out must not overlap y (OLLIE_EINVAL). */
+int ollie_eop_offset_sum(const ollie_conv_desc* desc, const void* y, int32_t y_dtype,
+                         void* out, void* stream);
+
+/* Selective-add eOperator of the transposed convolution alone (section 6.3): the same
+ * arguments, with the tap rule of derived_conv_transpose2d
+ *   th = ho + pad_h - r*dil_h, th >= 0, th % stride_h == 0, hi = th / stride_h < h. */
+int ollie_eop_convt_gather(const ollie_conv_desc* desc, const void* y, int32_t y_dtype,
+                           void* out, void* stream);
 
 /* Band stages alone (layouts as in banded_bmm):
- *   g2bmm:   S fp32 [b][l][2w+1] from Q, K
- *   softmax: P bf16 [b][l][2w+1] from S (flags: OLLIE_BAND_MASK_INVALID)
- *   gbmm:    O from P and V */
+ *   g2bmm:   the G2BMM of Table 2, S fp32 [b][l][2w+1] from Q, K (dilated band evaluated
+ *            per residue subsequence, section 6.4);
+ *   softmax: the row softmax eOperator, P bf16 [b][l][2w+1] from S (flags:
+ *            OLLIE_BAND_MASK_INVALID); 2w+1 <= 1024 (else OLLIE_EINVAL);
+ *   gbmm:    the band-times-dense product, O [b][l][d] (out_dtype) from P and V.
+ * Outputs must not overlap inputs (OLLIE_EINVAL). */
 int ollie_band_g2bmm(const ollie_band_desc* desc, const void* q, const void* k, float* s,
                      void* stream);
 int ollie_band_softmax(const ollie_band_desc* desc, const float* s, void* p, uint32_t flags,

@@ -20,7 +20,9 @@ import numpy as np
 from . import derived_form  # noqa: F401  (re-exported)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# OLLIE_ORACLE_LIBRARY names another build of oracle.c to load (the sanitizer test runs
+# the pins against an AddressSanitizer/UBSan build this way)
+_LIB_PATH = os.environ.get("OLLIE_ORACLE_LIBRARY") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 

@@ -2,8 +2,9 @@
 
 Argument marshalling only: every step of every operator runs in the library's HIP
 kernels.  torch provides device memory and the current HIP stream.  There is no CPU
-fallback: a missing libollie.so is built from csrc/ with hipcc on first use (and the
-call raises if that fails), and tensors that are not on a GPU raise.
+fallback: a missing libollie.so, or one built from sources other than those on disk
+(its build digest differs), is built from csrc/ with hipcc on first use (and the call
+raises if that fails), and tensors that are not on a GPU raise.
 
 Layouts (contiguous):
   x   [n][h][w][c] (NHWC)          wt  [r][s][k][c]  (torch conv2d weight .permute(2,3,0,1),
@@ -19,7 +20,10 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libollie.so")
+_DEFAULT_LIB = os.path.join(_HERE, "libollie.so")
+# OLLIE_LIBRARY names another build of the library to load (the sanitizer test runs the
+# host-side checks against an AddressSanitizer/UBSan build this way)
+LIB_PATH = os.environ.get("OLLIE_LIBRARY") or _DEFAULT_LIB
 
 OK, EINVAL, EDTYPE, EWORKSPACE, EALIGN, EHIP = range(6)
 F32, BF16 = 0, 1
@@ -30,14 +34,31 @@ BAND_MASK_INVALID = 1 << 3
 DILATED_RESIDUES = 1 << 4
 CONV_SPLIT_3X3 = 1 << 5
 
+
+def FUSED_TILE(n: int) -> int:
+    """Flag bits forcing tile shape n (0..14) of the fused convolution kernel."""
+    return ((n + 1) & 0xff) << 16
+
+
+def GEMM_TILE(n: int) -> int:
+    """Flag bits forcing tile shape n (0..4) of the GEMM stage kernel."""
+    return ((n + 1) & 0xf) << 24
+
+
+def BAND_SHAPE(n: int) -> int:
+    """Flag bits forcing wave shape n (0..2) of the fused band kernel."""
+    return ((n + 1) & 0xff) << 16
+
+
 _STATUS_NAMES = {OK: "OLLIE_OK", EINVAL: "OLLIE_EINVAL", EDTYPE: "OLLIE_EDTYPE",
                  EWORKSPACE: "OLLIE_EWORKSPACE", EALIGN: "OLLIE_EALIGN", EHIP: "OLLIE_EHIP"}
 
 EXPORTS = ("derived_conv2d", "derived_dilated_conv2d", "derived_conv_transpose2d", "banded_bmm",
-           "derived_conv2d_ex", "derived_dilated_conv2d_ex", "derived_conv_transpose2d_ex",
+           "ollie_derived_conv2d_ex", "ollie_derived_dilated_conv2d_ex",
+           "ollie_derived_conv_transpose2d_ex",
            "ollie_conv_out_hw", "ollie_conv_workspace_bytes", "ollie_band_workspace_bytes",
-           "ollie_last_error", "ollie_version", "ollie_gemm_nt", "ollie_eop_gather",
-           "ollie_band_g2bmm", "ollie_band_softmax", "ollie_band_gbmm")
+           "ollie_last_error", "ollie_version", "ollie_gemm_nt", "ollie_eop_offset_sum",
+           "ollie_eop_convt_gather", "ollie_band_g2bmm", "ollie_band_softmax", "ollie_band_gbmm")
 
 
 class ConvDesc(ctypes.Structure):
@@ -73,12 +94,13 @@ _lib = None
 
 
 def load_library(path: str = LIB_PATH):
-    """Load libollie.so (building it first only if it does not exist)."""
+    """Load libollie.so, building it first if it is missing or was built from other
+    sources than those now in csrc/ (its recorded build digest differs)."""
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(path):
-        from . import _build
+    from . import _build
+    if path == _DEFAULT_LIB and not _build.is_current():
         _build.build()
     lib = ctypes.CDLL(path)
     p, i64, i32, u32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32,
@@ -89,9 +111,9 @@ def load_library(path: str = LIB_PATH):
         "derived_conv2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
         "derived_dilated_conv2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
         "derived_conv_transpose2d": ([cdp, p, p, p, p, sz, u32, p], ctypes.c_int),
-        "derived_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
-        "derived_dilated_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
-        "derived_conv_transpose2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
+        "ollie_derived_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
+        "ollie_derived_dilated_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
+        "ollie_derived_conv_transpose2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
         "banded_bmm": ([bdp, p, p, p, p, p, p, sz, u32, p], ctypes.c_int),
         "ollie_conv_out_hw": ([cdp, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64)],
                               ctypes.c_int),
@@ -100,7 +122,8 @@ def load_library(path: str = LIB_PATH):
         "ollie_last_error": ([], ctypes.c_char_p),
         "ollie_version": ([], ctypes.c_char_p),
         "ollie_gemm_nt": ([i64, i64, i64, p, p, p, i32, i32, p], ctypes.c_int),
-        "ollie_eop_gather": ([cdp, ctypes.c_int, p, i32, p, p], ctypes.c_int),
+        "ollie_eop_offset_sum": ([cdp, p, i32, p, p], ctypes.c_int),
+        "ollie_eop_convt_gather": ([cdp, p, i32, p, p], ctypes.c_int),
         "ollie_band_g2bmm": ([bdp, p, p, p, p], ctypes.c_int),
         "ollie_band_softmax": ([bdp, p, p, u32, p], ctypes.c_int),
         "ollie_band_gbmm": ([bdp, p, p, p, p], ctypes.c_int),
@@ -219,7 +242,7 @@ def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output
         st = getattr(lib, entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out), _ptr(ws),
                                  ws_bytes, flags, _stream(x.device))
     else:
-        entry = entry + "_ex"
+        entry = "ollie_" + entry + "_ex"
         st = getattr(lib, entry)(ctypes.byref(desc), _ptr(x), _ptr(wt), _ptr(out), _ptr(ws),
                                  ws_bytes, flags, ctypes.byref(epi), _stream(x.device))
     _check(st, entry)
@@ -228,35 +251,37 @@ def _conv(entry: str, transposed: bool, x, wt, stride, padding, dilation, output
 
 def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=False,
                    out=None, ws=None, fuse=False, bias=None, residual=None, relu=False,
-                   split3x3=False):
+                   split3x3=False, flags=0):
     """Conv2d (dilation 1) as GEMM + OffsetAdd eOperator (fuse=True: the fused
     expression, no Y).  x [N,H,W,C], wt [R,S,K,C].  bias / residual / relu: an
     element-wise tail act(conv + bias + residual) evaluated in the last kernel.
     split3x3=True (stride 1): the R x S kernel as ceil(R/3) x ceil(S/3) blocks of a 3x3
     convolution (fused by `fuse` where covered) whose partial outputs an OffsetAdd with
-    offset step 3 sums (the Conv5x5 -> Conv3x3 derived form)."""
+    offset step 3 sums (the Conv5x5 -> Conv3x3 derived form).  flags: extra flag bits
+    (e.g. FUSED_TILE(n) / GEMM_TILE(n) tile overrides)."""
     return _conv("derived_conv2d", False, x, wt, stride, padding, 1, 0, out_dtype, y_bf16,
-                 out, ws, fuse, bias, residual, relu, CONV_SPLIT_3X3 if split3x3 else 0)
+                 out, ws, fuse, bias, residual, relu,
+                 (CONV_SPLIT_3X3 if split3x3 else 0) | flags)
 
 
 def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,
                            y_bf16=False, out=None, ws=None, fuse=False, bias=None,
-                           residual=None, relu=False, residues=False):
+                           residual=None, relu=False, residues=False, flags=0):
     """Dilated Conv2d as GEMM + dilated OffsetAdd eOperator.  residues=True (implies
     fuse=True) evaluates it as dil_h*dil_w non-dilated convolutions over the residue
-    sub-images of the input instead (stride 1)."""
+    sub-images of the input instead (stride 1).  flags: extra flag bits."""
     return _conv("derived_dilated_conv2d", False, x, wt, stride, padding, dilation, 0,
                  out_dtype, y_bf16, out, ws, fuse or residues, bias, residual, relu,
-                 DILATED_RESIDUES if residues else 0)
+                 (DILATED_RESIDUES if residues else 0) | flags)
 
 
 def derived_conv_transpose2d(x, wt, stride=1, padding=0, output_padding=0, dilation=1,
                              out_dtype=torch.float32, y_bf16=False, out=None, ws=None,
-                             fuse=False, bias=None, residual=None, relu=False):
+                             fuse=False, bias=None, residual=None, relu=False, flags=0):
     """ConvTranspose2d as GEMM on the unpadded input + selective-add eOperator.
-    x [N,H,W,C_in], wt [R,S,C_out,C_in]."""
+    x [N,H,W,C_in], wt [R,S,C_out,C_in].  flags: extra flag bits."""
     return _conv("derived_conv_transpose2d", True, x, wt, stride, padding, dilation,
-                 output_padding, out_dtype, y_bf16, out, ws, fuse, bias, residual, relu)
+                 output_padding, out_dtype, y_bf16, out, ws, fuse, bias, residual, relu, flags)
 
 
 def band_desc(q_shape, w, dilation, scale=1.0, out_dtype=torch.float32) -> BandDesc:
@@ -269,10 +294,12 @@ def band_workspace_bytes(desc: BandDesc, flags: int) -> int:
 
 
 def banded_bmm(q, k, v, w, dilation=1, scale=1.0, mask_invalid=False, staged=False,
-               out_dtype=torch.float32, return_s=False, out=None, ws=None, s_out=None):
+               out_dtype=torch.float32, return_s=False, out=None, ws=None, s_out=None,
+               flags=0):
     """Banded dilated batched matmul + softmax + band-times-dense (q, k, v [B,L,64] bf16).
 
-    Returns O, or (O, S) when return_s (staged path only)."""
+    Returns O, or (O, S) when return_s (staged path only).  flags: extra flag bits
+    (e.g. BAND_SHAPE(n))."""
     for t, name in ((q, "q"), (k, "k"), (v, "v")):
         _gpu(t, name)
         if t.dtype != torch.bfloat16:
@@ -280,7 +307,7 @@ def banded_bmm(q, k, v, w, dilation=1, scale=1.0, mask_invalid=False, staged=Fal
         if t.shape != q.shape:
             raise ValueError("q, k, v must have the same shape")
     desc = band_desc(tuple(q.shape), w, dilation, scale, out_dtype)
-    flags = (BAND_STAGED if staged or return_s else 0) | (BAND_MASK_INVALID if mask_invalid else 0)
+    flags |= (BAND_STAGED if staged or return_s else 0) | (BAND_MASK_INVALID if mask_invalid else 0)
     if out is None:
         out = torch.empty(tuple(q.shape), dtype=out_dtype, device=q.device)
     if return_s and s_out is None:
@@ -320,9 +347,10 @@ def eop_gather(desc: ConvDesc, transposed: bool, y, out=None):
     if out is None:
         out = torch.empty((desc.n, ho, wo, desc.k), dtype=_torch_dtype(desc.out_dtype),
                           device=y.device)
-    st = load_library().ollie_eop_gather(ctypes.byref(desc), int(transposed), _ptr(y),
-                                         _dtype_code(y.dtype), _ptr(out), _stream(y.device))
-    _check(st, "ollie_eop_gather")
+    entry = "ollie_eop_convt_gather" if transposed else "ollie_eop_offset_sum"
+    st = getattr(load_library(), entry)(ctypes.byref(desc), _ptr(y), _dtype_code(y.dtype),
+                                        _ptr(out), _stream(y.device))
+    _check(st, entry)
     return out
 
 

@@ -2,10 +2,16 @@
 
 Each .hip source is compiled for gfx950 only, then linked into one shared library
 next to this file.  Run ``python -m paper_2208_02025_amd._build`` or call build().
+
+Next to the library the build writes ``libollie.so.sha256``: a digest of every input
+of the build (sources, headers, flags).  The loader rebuilds when the digest of the
+sources on disk differs from it, so a stale binary is never used silently.
 """
 from __future__ import annotations
 
 import concurrent.futures as cf
+import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -15,6 +21,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJ_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libollie.so")
+STAMP = LIB + ".sha256"
+HEADER = os.path.join(os.path.dirname(HERE), "include", "ollie.h")
 SOURCES = ["abi.hip", "gemm.hip", "eop.hip", "band.hip", "conv_fused.hip", "split3.hip"]
 ARCH = "gfx950"
 
@@ -40,6 +48,28 @@ def _hipcc() -> str:
 SOURCE_FLAGS = {"conv_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
+def source_digest(csrc: str = CSRC, header: str = HEADER) -> str:
+    """sha256 over the build inputs: every file under csrc/, the public header and the
+    compiler flags (in a fixed order)."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(csrc, "*")))
+    for f in files + [header]:
+        h.update(os.path.basename(f).encode() + b"\0")
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+        h.update(b"\0")
+    h.update(repr((SOURCES, HIPCC_FLAGS, sorted(SOURCE_FLAGS.items()), ARCH)).encode())
+    return h.hexdigest()
+
+
+def is_current(lib: str = LIB, stamp: str = STAMP) -> bool:
+    """True when `lib` exists and was built from the sources now on disk."""
+    if not (os.path.exists(lib) and os.path.exists(stamp)):
+        return False
+    with open(stamp) as fh:
+        return fh.read().strip() == source_digest()
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o")
     cmd = [_hipcc(), *HIPCC_FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src),
@@ -53,6 +83,7 @@ def _compile(src: str, verbose: bool) -> str:
 
 
 def build(verbose: bool = False) -> str:
+    digest = source_digest()
     os.makedirs(OBJ_DIR, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
@@ -64,7 +95,51 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stderr}")
     os.replace(tmp, LIB)
+    with open(STAMP + ".tmp", "w") as fh:
+        fh.write(digest + "\n")
+    os.replace(STAMP + ".tmp", STAMP)
     return LIB
+
+
+def asan_runtime() -> str:
+    """The clang AddressSanitizer runtime that a process loading build_sanitized()'s
+    library must preload (the library itself does not link it)."""
+    res = subprocess.run([os.path.join(os.path.dirname(_hipcc()), "..", "llvm", "bin", "clang"),
+                          "-print-file-name=libclang_rt.asan-x86_64.so"],
+                         capture_output=True, text=True)
+    path = res.stdout.strip()
+    if res.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError("clang AddressSanitizer runtime not found")
+    return path
+
+
+def build_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """A copy of the library whose host code in abi.hip (argument validation, sizing,
+    dispatch) is built with AddressSanitizer and UndefinedBehaviorSanitizer; device
+    code is built as usual, and the other sources are the regular objects.  For CPU
+    tests of the host logic; load it with asan_runtime() preloaded."""
+    if not all(os.path.exists(os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".o"))
+               for s in SOURCES):
+        build(verbose)
+    os.makedirs(out_dir, exist_ok=True)
+    obj = os.path.join(out_dir, "abi_san.o")
+    san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+    cmd = [_hipcc(), *HIPCC_FLAGS, *san, "-c", os.path.join(CSRC, "abi.hip"), "-o", obj]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed on abi.hip (sanitized):\n{res.stderr}")
+    objs = [obj] + [os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".o")
+                    for s in SOURCES if s != "abi.hip"]
+    lib = os.path.join(out_dir, "libollie_san.so")
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Xarch_host",
+           "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-o", lib, *objs]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link failed (sanitized):\n{res.stderr}")
+    return lib
 
 
 if __name__ == "__main__":

@@ -28,6 +28,22 @@ int hip_fail(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Whether the byte ranges [a, a + na) and [b, b + nb) share a byte (null or empty
+// ranges share none).
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+// Tile-configuration override bits of the flags (0 = automatic, else config + 1).
+constexpr uint32_t kFusedTileBits = 0xffu << 16, kGemmTileBits = 0xfu << 24;
+constexpr uint32_t kBandShapeBits = 0xffu << 16;
+constexpr int kFusedTiles = 15, kGemmTiles = 5, kBandShapes = 3;
+int fused_tile(uint32_t flags) { return (int)((flags & kFusedTileBits) >> 16) - 1; }
+int gemm_tile(uint32_t flags) { return (int)((flags & kGemmTileBits) >> 24) - 1; }
+int band_shape(uint32_t flags) { return (int)((flags & kBandShapeBits) >> 16) - 1; }
+
 bool dtype_ok(int32_t d) { return d == OLLIE_F32 || d == OLLIE_BF16; }
 
 size_t dsize(int32_t d) { return d == OLLIE_BF16 ? 2 : 4; }
@@ -181,20 +197,36 @@ int check_gemm(int64_t m, int64_t n, int64_t k, const void* a, const void* b, co
     if (in_dtype == OLLIE_BF16 && (k % 8) != 0)
         return fail(OLLIE_EALIGN, "bf16 operands need k %% 8 == 0 (16-byte rows), got k=%lld",
                     (long long)k);
+    const size_t el = dsize(in_dtype), y_bytes = (size_t)(m * n) * dsize(y_dtype);
+    if (overlap(y, y_bytes, a, (size_t)(m * k) * el) || overlap(y, y_bytes, b, (size_t)(n * k) * el))
+        return fail(OLLIE_EINVAL, "y overlaps a or b");
     return OLLIE_OK;
 }
 
-// Validates an optional element-wise tail and converts it to the kernels' form.
-int make_epi(const ollie_conv_epilogue* e, Epi* out) {
-    *out = Epi{nullptr, nullptr, 0, 0, 0};
+// Validates an optional element-wise tail and converts it to the kernels' form.  The
+// residual may be the output buffer itself (same pointer and dtype: each element is read
+// and then written by one thread), but may not overlap it otherwise; the bias may not
+// overlap it at all.
+int make_epi(const ollie_conv_epilogue* e, const ollie_conv_desc* d, const void* out,
+             size_t out_bytes, Epi* ep) {
+    *ep = Epi{nullptr, nullptr, 0, 0, 0};
     if (!e) return OLLIE_OK;
     if (e->relu != 0 && e->relu != 1) return fail(OLLIE_EINVAL, "epilogue relu must be 0 or 1");
     if ((e->bias && !dtype_ok(e->bias_dtype)) || (e->residual && !dtype_ok(e->residual_dtype)))
         return fail(OLLIE_EDTYPE, "epilogue bias/residual dtype must be OLLIE_F32 or OLLIE_BF16");
     if (!aligned16(e->bias) || !aligned16(e->residual))
         return fail(OLLIE_EALIGN, "epilogue bias/residual pointers must be 16-byte aligned");
-    *out = Epi{e->bias, e->residual, e->bias_dtype == OLLIE_BF16,
-               e->residual_dtype == OLLIE_BF16, e->relu};
+    const size_t n_out = out_bytes / dsize(d->out_dtype);
+    if (overlap(e->bias, (size_t)d->k * dsize(e->bias_dtype), out, out_bytes))
+        return fail(OLLIE_EINVAL, "epilogue bias overlaps the output");
+    if (e->residual == out) {
+        if (e->residual_dtype != d->out_dtype)
+            return fail(OLLIE_EINVAL, "an in-place residual needs residual_dtype == out_dtype");
+    } else if (overlap(e->residual, n_out * dsize(e->residual_dtype), out, out_bytes)) {
+        return fail(OLLIE_EINVAL, "epilogue residual overlaps the output (other than in place)");
+    }
+    *ep = Epi{e->bias, e->residual, e->bias_dtype == OLLIE_BF16,
+              e->residual_dtype == OLLIE_BF16, e->relu};
     return OLLIE_OK;
 }
 
@@ -258,15 +290,33 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     int64_t ho, wo;
     int st = check_conv_geom(d, transposed, &ho, &wo);
     if (st) return st;
-    Epi epi;
-    st = make_epi(epilogue, &epi);
-    if (st) return st;
     if (flags & ~(uint32_t)(OLLIE_Y_BF16 | OLLIE_FUSE_EPILOGUE | OLLIE_DILATED_RESIDUES |
-                            OLLIE_CONV_SPLIT_3X3))
+                            OLLIE_CONV_SPLIT_3X3 | kFusedTileBits | kGemmTileBits))
         return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
+    if (fused_tile(flags) >= kFusedTiles || gemm_tile(flags) >= kGemmTiles)
+        return fail(OLLIE_EINVAL, "tile override out of range (fused 0..%d, GEMM 0..%d)",
+                    kFusedTiles - 1, kGemmTiles - 1);
     if (!x || !wt || !out) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!dtype_ok(d->in_dtype) || !dtype_ok(d->out_dtype))
         return fail(OLLIE_EDTYPE, "in_dtype/out_dtype must be OLLIE_F32 or OLLIE_BF16");
+    const size_t out_bytes = (size_t)(d->n * ho * wo * d->k) * dsize(d->out_dtype);
+    Epi epi;
+    st = make_epi(epilogue, d, out, out_bytes, &epi);
+    if (st) return st;
+    {
+        const size_t in_el = dsize(d->in_dtype);
+        const size_t x_bytes = (size_t)(d->n * d->h * d->w) * (size_t)d->c * in_el;
+        const size_t wt_bytes = (size_t)(d->r * d->s * d->k) * (size_t)d->c * in_el;
+        // the part of the workspace the call would use (a short one fails later, with
+        // OLLIE_EWORKSPACE)
+        size_t ws_used = ws ? conv_ws(d, transposed, ho, wo, flags) : 0;
+        ws_used = ws_used < ws_bytes ? ws_used : ws_bytes;
+        if (overlap(out, out_bytes, x, x_bytes) || overlap(out, out_bytes, wt, wt_bytes) ||
+            overlap(out, out_bytes, ws, ws_used))
+            return fail(OLLIE_EINVAL, "out overlaps x, wt or the workspace");
+        if (overlap(ws, ws_used, x, x_bytes) || overlap(ws, ws_used, wt, wt_bytes))
+            return fail(OLLIE_EINVAL, "the workspace overlaps x or wt");
+    }
     if (flags & OLLIE_CONV_SPLIT_3X3) {
         if (flags & OLLIE_DILATED_RESIDUES)
             return fail(OLLIE_EINVAL, "OLLIE_CONV_SPLIT_3X3 and OLLIE_DILATED_RESIDUES exclude "
@@ -283,7 +333,7 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
             return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
         hipError_t e = launch_conv_fused(conv_geom(d, ho, wo), conv_form(transposed, flags), x,
                                          wt, out, d->out_dtype == OLLIE_BF16, epi,
-                                         (hipStream_t)stream);
+                                         fused_tile(flags), (hipStream_t)stream);
         if (e != hipSuccess) return hip_fail(e, "fused GEMM+eOperator launch");
         return OLLIE_OK;
     }
@@ -300,7 +350,8 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     if (st) return st;
     hipStream_t s = (hipStream_t)stream;
     const int y_bf16 = (flags & OLLIE_Y_BF16) ? 1 : 0;
-    hipError_t e = launch_gemm_nt(m, nc, d->c, x, wt, ws, d->in_dtype == OLLIE_BF16, y_bf16, s);
+    hipError_t e = launch_gemm_nt(m, nc, d->c, x, wt, ws, d->in_dtype == OLLIE_BF16, y_bf16,
+                                  gemm_tile(flags), s);
     if (e != hipSuccess) return hip_fail(e, "GEMM stage launch");
     e = launch_eop_gather(conv_geom(d, ho, wo), transposed, ws, y_bf16, out,
                           d->out_dtype == OLLIE_BF16, epi, s);
@@ -341,6 +392,7 @@ size_t band_p_offset(const ollie_band_desc* d) { return (band_s_bytes(d) + 255) 
 size_t band_p_bytes(const ollie_band_desc* d) {
     return (size_t)(d->b * d->l) * (size_t)(2 * d->w + 1) * 2;
 }
+size_t band_qkv_bytes(const ollie_band_desc* d) { return (size_t)(d->b * d->l * d->d) * 2; }
 
 constexpr int64_t kSoftmaxMaxBand = 16 * 64;   // register-resident row length of the staged softmax
 
@@ -351,7 +403,7 @@ extern "C" {
 
 const char* ollie_last_error(void) { return g_err; }
 
-const char* ollie_version(void) { return "ollie-mi355x 0.1.0 (gfx950)"; }
+const char* ollie_version(void) { return "ollie-mi355x 0.2.0 (gfx950)"; }
 
 int ollie_conv_out_hw(const ollie_conv_desc* desc, int transposed, int64_t* ho, int64_t* wo) {
     g_err[0] = 0;
@@ -372,7 +424,7 @@ size_t ollie_band_workspace_bytes(const ollie_band_desc* desc, uint32_t flags) {
     return band_p_offset(desc) + band_p_bytes(desc);
 }
 
-int derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
+int ollie_derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                       void* ws, size_t ws_bytes, uint32_t flags,
                       const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
@@ -383,7 +435,7 @@ int derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt
     return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
 }
 
-int derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+int ollie_derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
                               void* out, void* ws, size_t ws_bytes, uint32_t flags,
                               const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
@@ -392,7 +444,7 @@ int derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const 
     return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
 }
 
-int derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
+int ollie_derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
                                 void* out, void* ws, size_t ws_bytes, uint32_t flags,
                                 const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
@@ -403,18 +455,18 @@ int derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x, cons
 
 int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                    void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
-    return derived_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
+    return ollie_derived_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
 }
 
 int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt,
                            void* out, void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
-    return derived_dilated_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
+    return ollie_derived_dilated_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
 }
 
 int derived_conv_transpose2d(const ollie_conv_desc* desc, const void* x, const void* wt,
                              void* out, void* ws, size_t ws_bytes, uint32_t flags,
                              void* stream) {
-    return derived_conv_transpose2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
+    return ollie_derived_conv_transpose2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
 }
 
 int banded_bmm(const ollie_band_desc* desc, const void* q, const void* k, const void* v,
@@ -422,18 +474,36 @@ int banded_bmm(const ollie_band_desc* desc, const void* q, const void* k, const 
     g_err[0] = 0;
     int st = check_band(desc);
     if (st) return st;
-    if (flags & ~(uint32_t)(OLLIE_BAND_STAGED | OLLIE_BAND_MASK_INVALID))
+    if (flags & ~(uint32_t)(OLLIE_BAND_STAGED | OLLIE_BAND_MASK_INVALID | kBandShapeBits))
         return fail(OLLIE_EINVAL, "unknown flag bits 0x%x", flags);
+    if (band_shape(flags) >= kBandShapes)
+        return fail(OLLIE_EINVAL, "band shape override out of range (0..%d)", kBandShapes - 1);
     if (!q || !k || !v || !o) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
         return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
     const int mask = (flags & OLLIE_BAND_MASK_INVALID) ? 1 : 0;
     const int o_bf16 = desc->out_dtype == OLLIE_BF16;
+    {
+        const size_t in_bytes = band_qkv_bytes(desc);
+        const size_t o_bytes = (size_t)(desc->b * desc->l * desc->d) * dsize(desc->out_dtype);
+        size_t ws_used = (flags & OLLIE_BAND_STAGED) && ws
+                             ? band_p_offset(desc) + band_p_bytes(desc) : 0;
+        ws_used = ws_used < ws_bytes ? ws_used : ws_bytes;
+        const size_t s_bytes = s_out ? band_s_bytes(desc) : 0;
+        const void* ins[3] = {q, k, v};
+        for (const void* t : ins)
+            if (overlap(o, o_bytes, t, in_bytes) || overlap(s_out, s_bytes, t, in_bytes) ||
+                overlap(ws, ws_used, t, in_bytes))
+                return fail(OLLIE_EINVAL, "o, s_out or the workspace overlaps q, k or v");
+        if (overlap(o, o_bytes, ws, ws_used) || overlap(o, o_bytes, s_out, s_bytes) ||
+            overlap(s_out, s_bytes, ws, ws_used))
+            return fail(OLLIE_EINVAL, "o, s_out and the workspace must not overlap");
+    }
     hipStream_t s = (hipStream_t)stream;
     BandGeom g = band_geom(desc);
     if (!(flags & OLLIE_BAND_STAGED)) {
         if (s_out) return fail(OLLIE_EINVAL, "s_out needs OLLIE_BAND_STAGED");
-        hipError_t e = launch_band_fused(g, q, k, v, o, o_bf16, mask, s);
+        hipError_t e = launch_band_fused(g, q, k, v, o, o_bf16, mask, band_shape(flags), s);
         if (e != hipSuccess) return hip_fail(e, "fused band launch");
         return OLLIE_OK;
     }
@@ -463,26 +533,48 @@ int ollie_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b,
     int st = check_gemm(m, n, k, a, b, y, in_dtype, y_dtype);
     if (st) return st;
     hipError_t e = launch_gemm_nt(m, n, k, a, b, y, in_dtype == OLLIE_BF16,
-                                  y_dtype == OLLIE_BF16, (hipStream_t)stream);
+                                  y_dtype == OLLIE_BF16, -1, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "GEMM launch");
     return OLLIE_OK;
 }
 
-int ollie_eop_gather(const ollie_conv_desc* desc, int transposed, const void* y,
-                     int32_t y_dtype, void* out, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int eop_stage(const ollie_conv_desc* desc, int transposed, const void* y, int32_t y_dtype,
+              void* out, void* stream) {
     g_err[0] = 0;
     int64_t ho, wo;
-    int st = check_conv_geom(desc, transposed ? 1 : 0, &ho, &wo);
+    int st = check_conv_geom(desc, transposed, &ho, &wo);
     if (st) return st;
     if (!y || !out) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!dtype_ok(y_dtype) || !dtype_ok(desc->out_dtype)) return fail(OLLIE_EDTYPE, "unknown dtype");
     if (!aligned16(y) || !aligned16(out))
         return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
-    hipError_t e = launch_eop_gather(conv_geom(desc, ho, wo), transposed ? 1 : 0, y,
+    const size_t y_bytes = (size_t)(desc->n * desc->h * desc->w) *
+                           (size_t)(desc->r * desc->s * desc->k) * dsize(y_dtype);
+    if (overlap(out, (size_t)(desc->n * ho * wo * desc->k) * dsize(desc->out_dtype), y, y_bytes))
+        return fail(OLLIE_EINVAL, "out overlaps y");
+    hipError_t e = launch_eop_gather(conv_geom(desc, ho, wo), transposed, y,
                                      y_dtype == OLLIE_BF16, out, desc->out_dtype == OLLIE_BF16,
                                      Epi{nullptr, nullptr, 0, 0, 0}, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "eOperator launch");
     return OLLIE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ollie_eop_offset_sum(const ollie_conv_desc* desc, const void* y, int32_t y_dtype,
+                         void* out, void* stream) {
+    return eop_stage(desc, 0, y, y_dtype, out, stream);
+}
+
+int ollie_eop_convt_gather(const ollie_conv_desc* desc, const void* y, int32_t y_dtype,
+                           void* out, void* stream) {
+    return eop_stage(desc, 1, y, y_dtype, out, stream);
 }
 
 int ollie_band_g2bmm(const ollie_band_desc* desc, const void* q, const void* k, float* s,
@@ -493,6 +585,9 @@ int ollie_band_g2bmm(const ollie_band_desc* desc, const void* q, const void* k, 
     if (!q || !k || !s) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!aligned16(q) || !aligned16(k) || !aligned16(s))
         return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    if (overlap(s, band_s_bytes(desc), q, band_qkv_bytes(desc)) ||
+        overlap(s, band_s_bytes(desc), k, band_qkv_bytes(desc)))
+        return fail(OLLIE_EINVAL, "s overlaps q or k");
     hipError_t e = launch_band_g2bmm(band_geom(desc), q, k, s, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "G2BMM launch");
     return OLLIE_OK;
@@ -510,6 +605,8 @@ int ollie_band_softmax(const ollie_band_desc* desc, const float* s, void* p, uin
         return fail(OLLIE_EINVAL, "softmax stage needs 2w+1 <= %lld", (long long)kSoftmaxMaxBand);
     if (!aligned16(s) || !aligned16(p))
         return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    if (overlap(p, band_p_bytes(desc), s, band_s_bytes(desc)))
+        return fail(OLLIE_EINVAL, "p overlaps s");
     hipError_t e = launch_band_softmax(band_geom(desc), s, p,
                                        (flags & OLLIE_BAND_MASK_INVALID) ? 1 : 0,
                                        (hipStream_t)stream);
@@ -525,6 +622,9 @@ int ollie_band_gbmm(const ollie_band_desc* desc, const void* p, const void* v, v
     if (!p || !v || !o) return fail(OLLIE_EINVAL, "null tensor pointer");
     if (!aligned16(p) || !aligned16(v) || !aligned16(o))
         return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+    const size_t o_bytes = (size_t)(desc->b * desc->l * desc->d) * dsize(desc->out_dtype);
+    if (overlap(o, o_bytes, p, band_p_bytes(desc)) || overlap(o, o_bytes, v, band_qkv_bytes(desc)))
+        return fail(OLLIE_EINVAL, "o overlaps p or v");
     hipError_t e = launch_band_gbmm(band_geom(desc), p, v, o, desc->out_dtype == OLLIE_BF16,
                                     (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "GBMM launch");

@@ -22,8 +22,6 @@
 // each 16-lane group receives element i%4 of the 8-byte rows addressed by lanes
 // i/4 + 4j (j = 0..3): lanes address rows (keys) and 4-column slices, the hardware
 // returns one column (value dimension) across four keys.
-#include <stdlib.h>
-
 #include <type_traits>
 
 #include "common.h"
@@ -751,12 +749,11 @@ hipError_t launch_fused_nw(const BandGeom& g, const void* q, const void* k, cons
 // Wave shapes: 0 = four waves of 32 queries (the default: measured faster than eight
 // waves, which have half the copies per query but the same occupancy and twice the LDS
 // per workgroup), 1 = four waves of 64 queries, 2 = two waves of 64 queries (half the
-// LDS reads per score, two waves per SIMD).  OLLIE_BAND_CONFIG overrides the choice
-// (read per call; sweeps and tests).
+// LDS reads per score, two waves per SIMD).  `shape` (0..2, from the caller's flags;
+// -1 = automatic) overrides the choice for tuning sweeps and tests.
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
-                             void* o, int o_bf16, int mask, hipStream_t stream) {
-    const char* env = getenv("OLLIE_BAND_CONFIG");
-    const int cfg = env ? atoi(env) : 0;
+                             void* o, int o_bf16, int mask, int shape, hipStream_t stream) {
+    const int cfg = shape < 0 ? 0 : shape;
     if (cfg == 1) return launch_fused_nw<4, 4>(g, q, k, v, o, o_bf16, mask, stream);
     if (cfg == 2) return launch_fused_nw<2, 4>(g, q, k, v, o, o_bf16, mask, stream);
     return launch_fused_nw<4, 2>(g, q, k, v, o, o_bf16, mask, stream);

@@ -138,8 +138,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 // ---------------------------------------------------------------- launchers
 // Each returns the hipError_t of the launch.
 
+// `tile` / `shape` arguments: a forced tile configuration of the kernel (tuning sweeps
+// and tests), or -1 for the automatic choice.
 hipError_t launch_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b,
-                          void* y, int in_bf16, int y_bf16, hipStream_t stream);
+                          void* y, int in_bf16, int y_bf16, int tile, hipStream_t stream);
 
 struct ConvGeom {
     int64_t n, c, h, w, k, r, s, ho, wo;
@@ -157,7 +159,8 @@ hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, i
 enum ConvForm { kForward = 0, kTransposed = 1, kResidues = 2 };
 bool conv_fused_supported(const ConvGeom& g, int form);
 hipError_t launch_conv_fused(const ConvGeom& g, int form, const void* x, const void* wt,
-                             void* out, int out_bf16, const Epi& epi, hipStream_t stream);
+                             void* out, int out_bf16, const Epi& epi, int tile,
+                             hipStream_t stream);
 
 // Weight blocks of the R x S -> 3x3 derived form: W3 [3][3][ceil(R/3)*ceil(S/3)*K][C]
 // from Wt [R][S][K][C] (g.r, g.s, g.k, g.c), zero where a block overhangs the kernel.
@@ -177,6 +180,6 @@ hipError_t launch_band_softmax(const BandGeom& g, const float* s, void* p, int m
 hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, void* o,
                             int o_bf16, hipStream_t stream);
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
-                             void* o, int o_bf16, int mask, hipStream_t stream);
+                             void* o, int o_bf16, int mask, int shape, hipStream_t stream);
 
 }  // namespace ollie

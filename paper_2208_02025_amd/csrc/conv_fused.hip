@@ -26,8 +26,6 @@
 // Main loop: the bf16 DMA pipeline of the GEMM stage (global_load_lds_dwordx4 into an
 // XOR-swizzled LDS ring, v_mfma_f32_16x16x32_bf16).  A rows are gathered per tap; rows
 // whose input pixel lies in the zero padding fetch a 16-byte zero chunk instead.
-#include <stdlib.h>
-
 #include "common.h"
 
 namespace ollie {
@@ -720,14 +718,12 @@ hipError_t go_window(FusedPlan& P, const void* x, const void* wt, void* out, con
 // 65-68 vs 68-69 us for 0, 12.2 vs 13.8 us and 11.3 vs 12.9 us for 6).  The row-window
 // kernel copies 35% fewer bytes on the CSRNet layer in the residue form but measured no
 // faster than 0 there (its copies overlap less with the MFMA work), so it is selected
-// only on request.  OLLIE_FUSED_CONFIG overrides the choice (tuning sweeps, tests); 9
-// falls back to the automatic choice where the row-window form does not apply.
+// only on request.  `forced` (0..14, from the caller's flags; -1 = automatic) overrides
+// the choice for tuning sweeps and tests; 9 falls back to the automatic choice where
+// the row-window form does not apply.
 template <typename OT>
 hipError_t dispatch(FusedPlan& P, const void* x, const void* wt, void* out, const Epi& epi,
-                    hipStream_t st) {
-    // read per call, so that a process can switch tile shapes between calls
-    const char* env = getenv("OLLIE_FUSED_CONFIG");
-    const int forced = env ? atoi(env) : -1;
+                    int forced, hipStream_t st) {
     // tensors of 2 GiB or more: 64-bit addressing (buffer offsets are 32-bit)
     if (P.x_bytes == 0 || P.w_bytes == 0) return go<128, 128, 2, OT, 8, false>(P, x, wt, out, epi, st);
     int cfg = forced;
@@ -781,11 +777,12 @@ bool conv_fused_supported(const ConvGeom& g, int form) {
 }
 
 hipError_t launch_conv_fused(const ConvGeom& g, int form, const void* x, const void* wt,
-                             void* out, int out_bf16, const Epi& epi, hipStream_t stream) {
+                             void* out, int out_bf16, const Epi& epi, int tile,
+                             hipStream_t stream) {
     FusedPlan P;
     if (g.c % kTileK != 0 || !make_plan(g, form, P)) return hipErrorInvalidValue;
-    return out_bf16 ? dispatch<bf16_t>(P, x, wt, out, epi, stream)
-                    : dispatch<float>(P, x, wt, out, epi, stream);
+    return out_bf16 ? dispatch<bf16_t>(P, x, wt, out, epi, tile, stream)
+                    : dispatch<float>(P, x, wt, out, epi, tile, stream);
 }
 
 }  // namespace ollie

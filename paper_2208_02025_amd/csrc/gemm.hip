@@ -25,8 +25,6 @@
 //
 // The MFMA is issued as D = Wt-tile x X-tile^T so that each lane ends up holding four
 // consecutive output columns n of one row m.
-#include <stdlib.h>
-
 #include <type_traits>
 
 #include "common.h"
@@ -136,6 +134,10 @@ __device__ __forceinline__ void store_tile_rows(YT* __restrict__ Y, const f32x4 
                     u[2] = (uint32_t)f2bf(v1[0]) | ((uint32_t)f2bf(v1[1]) << 16);
                     u[3] = (uint32_t)f2bf(v1[2]) | ((uint32_t)f2bf(v1[3]) << 16);
                     *reinterpret_cast<u32x4*>(dst) = u;
+                } else if (vec_ok) {
+                    // N % 4 == 0: whole 4-value halves are in or out of the row
+                    if (n + 3 < N) Out<YT>::put4(dst, v0);
+                    if (n + 7 < N) Out<YT>::put4(dst + 4, v1);
                 } else {
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
@@ -424,11 +426,10 @@ hipError_t go_dma(int64_t m, int64_t n, int64_t k, const void* a, const void* b,
 //   0 = 128x128, 4 waves, 2 stages, two per CU      1 = 128x128, 8 waves, 2 stages, two per CU
 //   2 = 64x128, 4 waves, 2 stages, three per CU     3 = 128x128, 4 waves, 3 stages, one per CU
 //   4 = 256x128, 8 waves, 2 stages, one per CU
-// OLLIE_GEMM_CONFIG (0..4, read per call) overrides the shape-based choice.
+// `forced` (0..4, from the caller's flags; -1 = automatic) overrides the shape-based
+// choice for tuning sweeps and tests.
 constexpr int kGemmConfigs = 5;
-int pick_config(int64_t m, int64_t n) {
-    const char* e = getenv("OLLIE_GEMM_CONFIG");
-    const int forced = e ? atoi(e) : -1;
+int pick_config(int64_t m, int64_t n, int forced) {
     if (forced >= 0 && forced < kGemmConfigs) return forced;
     // up to one 128x128 tile per CU: halve the tile height to give every CU work
     const int64_t t128 = ((m + 127) / 128) * ((n + 127) / 128);
@@ -437,12 +438,12 @@ int pick_config(int64_t m, int64_t n) {
 
 template <typename YT>
 hipError_t go_bf16(int64_t m, int64_t n, int64_t k, const void* a, const void* b, void* y,
-                   hipStream_t stream) {
+                   int tile, hipStream_t stream) {
     if (k % kBK == 0) {
         // buffer offsets are 32-bit: larger operands take the 64-bit address form
         if (m * k * 2 >= (int64_t(1) << 31) || n * k * 2 >= (int64_t(1) << 31))
             return go_dma<128, 128, 2, 2, 2, 2, false, YT>(m, n, k, a, b, y, stream);
-        switch (pick_config(m, n)) {
+        switch (pick_config(m, n, tile)) {
         case 1: return go_dma<128, 128, 2, 2, 4, 2, true, YT>(m, n, k, a, b, y, stream);
         case 2: return go_dma<64, 128, 2, 2, 2, 3, true, YT>(m, n, k, a, b, y, stream);
         case 3: return go_dma<128, 128, 3, 2, 2, 1, true, YT>(m, n, k, a, b, y, stream);
@@ -469,10 +470,10 @@ hipError_t go_f32(int64_t m, int64_t n, int64_t k, const void* a, const void* b,
 }  // namespace
 
 hipError_t launch_gemm_nt(int64_t m, int64_t n, int64_t k, const void* a, const void* b,
-                          void* y, int in_bf16, int y_bf16, hipStream_t stream) {
+                          void* y, int in_bf16, int y_bf16, int tile, hipStream_t stream) {
     if (in_bf16)
-        return y_bf16 ? go_bf16<bf16_t>(m, n, k, a, b, y, stream)
-                      : go_bf16<float>(m, n, k, a, b, y, stream);
+        return y_bf16 ? go_bf16<bf16_t>(m, n, k, a, b, y, tile, stream)
+                      : go_bf16<float>(m, n, k, a, b, y, tile, stream);
     return y_bf16 ? go_f32<bf16_t>(m, n, k, a, b, y, stream)
                   : go_f32<float>(m, n, k, a, b, y, stream);
 }

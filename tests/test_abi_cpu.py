@@ -17,7 +17,8 @@ A16 = ctypes.c_void_p(0x10000)
 B16 = ctypes.c_void_p(0x20000)
 C16 = ctypes.c_void_p(0x30000)
 W16 = ctypes.c_void_p(0x40000)
-MIS = ctypes.c_void_p(0x10008)
+MIS = ctypes.c_void_p(0x2000008)   # misaligned, clear of the other fake tensors
+WSB = ctypes.c_void_p(0x1000000)   # a band workspace clear of the fake tensors above
 
 
 def header_functions():
@@ -137,8 +138,8 @@ def test_band_error_paths(lib):
         (band(), {"s_out": C16}, ol.EINVAL),                        # s_out needs the staged path
         (band(), {"flags": 1 << 7}, ol.EINVAL),
         (band(), {"flags": ol.BAND_STAGED}, ol.EINVAL),             # staged without workspace
-        (band(), {"flags": ol.BAND_STAGED, "ws": W16, "ws_bytes": 100}, ol.EWORKSPACE),
-        (band(w=600), {"flags": ol.BAND_STAGED, "ws": W16, "ws_bytes": 1 << 40}, ol.EINVAL),
+        (band(), {"flags": ol.BAND_STAGED, "ws": WSB, "ws_bytes": 100}, ol.EWORKSPACE),
+        (band(w=600), {"flags": ol.BAND_STAGED, "ws": WSB, "ws_bytes": 1 << 40}, ol.EINVAL),
     ]
     for d, kw, want in cases:
         st, msg = call(d, **kw)
@@ -175,8 +176,11 @@ def test_gemm_error_paths(lib):
 
 def test_stage_error_paths(lib):
     d = conv()
-    assert lib.ollie_eop_gather(ctypes.byref(d), 0, None, ol.F32, C16, None) == ol.EINVAL
-    assert lib.ollie_eop_gather(ctypes.byref(d), 0, A16, 5, C16, None) == ol.EDTYPE
+    for entry in ("ollie_eop_offset_sum", "ollie_eop_convt_gather"):
+        fn = getattr(lib, entry)
+        assert fn(ctypes.byref(d), None, ol.F32, C16, None) == ol.EINVAL
+        assert fn(ctypes.byref(d), A16, 5, C16, None) == ol.EDTYPE
+        assert fn(ctypes.byref(d), A16, ol.F32, MIS, None) == ol.EALIGN
     bd = band()
     assert lib.ollie_band_g2bmm(ctypes.byref(bd), A16, None, C16, None) == ol.EINVAL
     assert lib.ollie_band_softmax(ctypes.byref(bd), A16, MIS, 0, None) == ol.EALIGN
@@ -216,7 +220,7 @@ def test_epilogue_error_paths(lib):
         st = getattr(lib, entry)(ctypes.byref(d), A16, B16, C16, W16, 1 << 40, 0,
                                  ctypes.byref(e), None)
         return st, lib.ollie_last_error().decode()
-    for entry in ("derived_conv2d_ex", "derived_dilated_conv2d_ex"):
+    for entry in ("ollie_derived_conv2d_ex", "ollie_derived_dilated_conv2d_ex"):
         assert call(entry, relu=2)[0] == ol.EINVAL
         assert call(entry, bias_dtype=7)[0] == ol.EDTYPE
         assert call(entry, residual=C16.value, residual_dtype=5)[0] == ol.EDTYPE
@@ -227,12 +231,12 @@ def test_epilogue_error_paths(lib):
     # a NULL tensor's dtype is not looked at
     dt = conv(stride=2)
     e = ol.ConvEpilogue(None, None, 9, 9, 0)
-    st = lib.derived_conv_transpose2d_ex(ctypes.byref(dt), A16, B16, C16, W16, 10, 0,
-                                         ctypes.byref(e), None)
+    st = lib.ollie_derived_conv_transpose2d_ex(ctypes.byref(dt), A16, B16, C16, W16, 10, 0,
+                                               ctypes.byref(e), None)
     assert st == ol.EWORKSPACE          # the epilogue passed; the workspace check fired
     # the plain entry points are the _ex ones with no tail
-    st = lib.derived_conv2d_ex(ctypes.byref(conv(dil=2, pad=2)), A16, B16, C16, W16, 1 << 40,
-                               0, None, None)
+    st = lib.ollie_derived_conv2d_ex(ctypes.byref(conv(dil=2, pad=2)), A16, B16, C16, W16,
+                                     1 << 40, 0, None, None)
     assert st == ol.EINVAL
 
 
@@ -310,3 +314,109 @@ def test_validation_never_lets_a_bad_descriptor_through(lib):
             st, msg = call_conv(lib, entry, d)
             assert st != ol.OK and msg, (entry, st)
     assert bad > 100
+
+
+def test_tile_override_bits(lib):
+    """Tile-configuration flag bits: in range they pass validation (the call then fails
+    later on the deliberately short workspace), out of range they give OLLIE_EINVAL."""
+    d = conv(c=64)
+    for fl in (ol.FUSED_TILE(0), ol.FUSED_TILE(14), ol.GEMM_TILE(0), ol.GEMM_TILE(4)):
+        assert call_conv(lib, "derived_conv2d", d, ws_bytes=8, flags=fl)[0] == ol.EWORKSPACE
+    for fl in (ol.FUSED_TILE(15), ol.FUSED_TILE(200), ol.GEMM_TILE(5), ol.GEMM_TILE(14)):
+        st, msg = call_conv(lib, "derived_conv2d", d, flags=fl)
+        assert st == ol.EINVAL and "tile" in msg
+    assert call_conv(lib, "derived_conv2d", d, flags=1 << 30)[0] == ol.EINVAL  # unknown bit
+    bd = band()
+    def bcall(flags, ws_bytes=0):
+        return lib.banded_bmm(ctypes.byref(bd), A16, B16, C16, W16, None, WSB, ws_bytes,
+                              flags, None)
+    assert bcall(ol.BAND_SHAPE(3)) == ol.EINVAL
+    assert bcall(ol.BAND_STAGED | ol.BAND_SHAPE(2), ws_bytes=8) == ol.EWORKSPACE
+    assert bcall(ol.GEMM_TILE(0)) == ol.EINVAL                # not a band flag
+
+
+def test_overlapping_buffers_are_rejected(lib):
+    """Outputs may not overlap inputs or the workspace (OLLIE_EINVAL); a residual may be
+    the output buffer itself (same dtype) but may not overlap it otherwise."""
+    d = conv(c=64, k=32)                      # x 25088 B, wt 36864 B, out 25088 B (fp32)
+    x, wt, out, ws = 0x100000, 0x200000, 0x300000, 0x400000
+    P = ctypes.c_void_p
+    def c(**kw):
+        a = dict(x=x, wt=wt, out=out, ws=ws)
+        a.update(kw)
+        return call_conv(lib, "derived_conv2d", d, P(a["x"]), P(a["wt"]), P(a["out"]),
+                         P(a["ws"]), 1 << 30)
+    assert c(out=x + 1024)[0] == ol.EINVAL              # out inside x
+    assert c(out=wt - 1024)[0] == ol.EINVAL             # out runs into wt
+    assert c(out=ws + 4096)[0] == ol.EINVAL             # out inside the workspace
+    assert c(ws=x + 4096)[0] == ol.EINVAL               # workspace over x
+    st, msg = c(x=out)
+    assert st == ol.EINVAL and "overlap" in msg
+    # epilogue aliasing
+    def e(bias, res, res_dtype=ol.F32):
+        ep = ol.ConvEpilogue(bias, res, ol.F32, res_dtype, 0)
+        st = lib.ollie_derived_conv2d_ex(ctypes.byref(d), P(x), P(wt), P(out), P(ws), 8, 0,
+                                         ctypes.byref(ep), None)
+        return st, lib.ollie_last_error().decode()
+    assert e(None, out)[0] == ol.EWORKSPACE              # in place: allowed
+    assert e(None, out, ol.BF16)[0] == ol.EINVAL         # in place with another dtype
+    assert e(None, out + 16)[0] == ol.EINVAL             # shifted residual
+    assert e(out + 64, None)[0] == ol.EINVAL             # bias inside out
+    assert e(out - 64, None)[0] == ol.EINVAL             # 32 fp32 bias values run into out
+    assert e(out - 128, out - (1 << 20))[0] == ol.EWORKSPACE
+    # GEMM stage, eOperator stage, band
+    assert lib.ollie_gemm_nt(64, 64, 64, P(x), P(wt), P(x + 4096), ol.BF16, ol.F32,
+                             None) == ol.EINVAL
+    assert lib.ollie_eop_offset_sum(ctypes.byref(conv()), P(x), ol.F32, P(x + 16), None) == \
+        ol.EINVAL
+    bd = band(b=1, l=64)                                  # q/k/v 8 KB each, O fp32 16 KB
+    def b(q, k, v, o, flags=0, ws_=None, ws_bytes=0, s_out=None):
+        return lib.banded_bmm(ctypes.byref(bd), P(q), P(k), P(v), P(o), P(s_out), P(ws_),
+                              ws_bytes, flags, None)
+    assert b(x, wt, out, x + 4096) == ol.EINVAL          # o over q
+    assert b(x, wt, out, ws, ol.BAND_STAGED, ws, 1 << 30) == ol.EINVAL   # o over ws
+    assert b(x, wt, out, ws, ol.BAND_STAGED, ws + (1 << 20), 1 << 30, s_out=out + 32) == \
+        ol.EINVAL                                        # s_out over v
+    assert lib.ollie_band_gbmm(ctypes.byref(bd), P(x), P(wt), P(x + 64), None) == ol.EINVAL
+    assert lib.ollie_band_softmax(ctypes.byref(bd), P(x), P(x + 64), 0, None) == ol.EINVAL
+    assert lib.ollie_band_g2bmm(ctypes.byref(bd), P(x), P(wt), P(wt + 64), None) == ol.EINVAL
+
+
+def test_build_digest_tracks_the_sources(tmp_path):
+    """The digest stored beside libollie.so covers every source, the header and the
+    flags: editing any of them changes it."""
+    import shutil
+    from paper_2208_02025_amd import _build
+    csrc = tmp_path / "csrc"
+    shutil.copytree(_build.CSRC, csrc)
+    hdr = tmp_path / "ollie.h"
+    shutil.copy(_build.HEADER, hdr)
+    base = _build.source_digest(str(csrc), str(hdr))
+    assert base == _build.source_digest(str(csrc), str(hdr))
+    assert base == _build.source_digest()                 # same content, other place
+    src = csrc / "eop.hip"
+    src.write_text(src.read_text() + "\n// edit\n")
+    assert _build.source_digest(str(csrc), str(hdr)) != base
+    src.write_text(src.read_text()[: -len("\n// edit\n")])
+    assert _build.source_digest(str(csrc), str(hdr)) == base
+    hdr.write_text(hdr.read_text().replace("OLLIE_OK = 0", "OLLIE_OK = 0 "))
+    assert _build.source_digest(str(csrc), str(hdr)) != base
+
+
+def test_stale_library_is_rebuilt(tmp_path, monkeypatch):
+    """A library whose recorded digest differs from the sources is not current, and
+    load_library() then rebuilds before loading."""
+    from paper_2208_02025_amd import _build
+    lib, stamp = tmp_path / "libx.so", tmp_path / "libx.so.sha256"
+    lib.write_bytes(b"")
+    assert not _build.is_current(str(lib), str(stamp))      # no stamp
+    stamp.write_text("0" * 64 + "\n")
+    assert not _build.is_current(str(lib), str(stamp))      # stale stamp
+    stamp.write_text(_build.source_digest() + "\n")
+    assert _build.is_current(str(lib), str(stamp))
+    calls = []
+    monkeypatch.setattr(ol, "_lib", None)
+    monkeypatch.setattr(_build, "is_current", lambda *a: False)
+    monkeypatch.setattr(_build, "build", lambda *a, **k: calls.append(1) or _build.LIB)
+    ol.load_library()
+    assert calls == [1]

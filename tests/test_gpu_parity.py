@@ -290,16 +290,37 @@ GEMM_CONFIGS = 5
 
 @pytest.mark.parametrize("cfg", range(GEMM_CONFIGS))
 @pytest.mark.parametrize("m,n,k", [(129, 257, 128), (300, 130, 192), (1000, 522, 64),
-                                   (64, 64, 512), (260, 1030, 256)])
+                                   (64, 64, 512), (260, 1030, 256), (300, 136, 128),
+                                   (129, 260, 64)])
 @pytest.mark.parametrize("y_bf16", [False, True])
-def test_gemm_every_tile_config_integer_exact(monkeypatch, cfg, m, n, k, y_bf16):
-    """Every DMA tile configuration on integer inputs: exact fp32 Y, and a bf16 Y equal
-    to the exact sum rounded to nearest even (n = 522 is not a multiple of 4, so the
-    row stores take their element-wise tail)."""
-    monkeypatch.setenv("OLLIE_GEMM_CONFIG", str(cfg))
+def test_gemm_every_tile_config_integer_exact(cfg, m, n, k, y_bf16):
+    """Every DMA tile configuration (flag bits GEMM_TILE(cfg)) of the GEMM stage, run as
+    the two-stage path of a 1x1 convolution (x [1,1,m,k], wt [1,1,n,k]), whose OffsetAdd
+    is the identity, so out = Y: exact for an fp32 Y, and for a bf16 Y equal to the exact
+    sum rounded to nearest even.  n = 522 is not a multiple of 4 (element-wise row
+    stores); n = 136 and 260 are multiples of 4 and 8 or 4 only with a ragged last tile
+    (16-byte and 8-byte bf16 row stores)."""
     say("gemm cfg", cfg, m, n, k, "bf16 y" if y_bf16 else "fp32 y")
     a = synth.random_tensor((m, k), 6100 + m, "bf16", integer=True)
     b = synth.random_tensor((n, k), 7100 + n, "bf16", integer=True)
+    out = ol.derived_conv2d(a.view(1, 1, m, k).to(DEV), b.view(1, 1, n, k).to(DEV), 1, 0,
+                            y_bf16=y_bf16, flags=ol.GEMM_TILE(cfg))
+    torch.cuda.synchronize()
+    ref = a.double().numpy() @ b.double().numpy().T
+    got = out.view(m, n).cpu()
+    if y_bf16:
+        assert torch.equal(got, torch.from_numpy(ref).to(torch.bfloat16).float())
+    else:
+        assert np.array_equal(got.numpy().astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("m,n,k", [(129, 257, 128), (300, 136, 64)])
+@pytest.mark.parametrize("y_bf16", [False, True])
+def test_gemm_stage_entry_point_integer_exact(m, n, k, y_bf16):
+    """ollie_gemm_nt itself (automatic tile choice) on integer inputs."""
+    say("gemm stage entry", m, n, k, y_bf16)
+    a = synth.random_tensor((m, k), 6150 + m, "bf16", integer=True)
+    b = synth.random_tensor((n, k), 7150 + n, "bf16", integer=True)
     y = ol.gemm_nt(a.to(DEV), b.to(DEV), y_dtype=torch.bfloat16 if y_bf16 else torch.float32)
     torch.cuda.synchronize()
     ref = a.double().numpy() @ b.double().numpy().T
@@ -328,15 +349,47 @@ def test_gemm_stage_operand_over_2gib_sampled():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("m,n,k", [(1, 1, 1), (70, 33, 17), (200, 100, 45)])
-def test_gemm_stage_fp32(m, n, k):
-    say("gemm fp32", m, n, k)
+@pytest.mark.parametrize("m,n,k", [(1, 1, 1), (70, 33, 17), (200, 100, 45), (130, 136, 64)])
+@pytest.mark.parametrize("y_bf16", [False, True])
+def test_gemm_stage_fp32(m, n, k, y_bf16):
+    """fp32 operands (the fp32 MFMA kernel) with an fp32 Y (<= 1e-5) and a bf16 Y
+    (<= the bf16 tolerance; on integer inputs exactly the RNE rounding of the sum)."""
+    say("gemm fp32", m, n, k, "bf16 y" if y_bf16 else "fp32 y")
+    yd = torch.bfloat16 if y_bf16 else torch.float32
     a = synth.random_tensor((m, k), 8000 + m)
     b = synth.random_tensor((n, k), 9000 + n)
-    y = ol.gemm_nt(a.to(DEV), b.to(DEV))
+    y = ol.gemm_nt(a.to(DEV), b.to(DEV), y_dtype=yd)
     torch.cuda.synchronize()
+    assert y.dtype == yd
     ref = a.double().numpy() @ b.double().numpy().T
-    assert err(to_np(y), ref) <= TOL_F32
+    assert err(to_np(y), ref) <= (TOL_BF16 if y_bf16 else TOL_F32)
+    ai = synth.random_tensor((m, k), 8100 + m, integer=True)
+    bi = synth.random_tensor((n, k), 9100 + n, integer=True)
+    y = ol.gemm_nt(ai.to(DEV), bi.to(DEV), y_dtype=yd)
+    torch.cuda.synchronize()
+    ref = torch.from_numpy(ai.double().numpy() @ bi.double().numpy().T).to(yd)
+    assert torch.equal(y.cpu(), ref)
+
+
+@pytest.mark.parametrize("integer", [True, False])
+def test_fp32_conv_with_bf16_scope(integer):
+    """fp32 inputs with OLLIE_Y_BF16 (the fp32 GEMM kernel storing a bf16 scope): the
+    tiny 3x3 workload and a ragged strided shape, against the oracle within the bf16
+    tolerance (bf16 Y carries the bf16 rounding of every partial)."""
+    wl = synth.WORKLOADS[1]
+    say("fp32 conv, bf16 Y, integer", integer)
+    x, wt = synth.conv_inputs(wl, integer=integer)
+    out = run_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil, y_bf16=True)
+    ref = oracle_conv(wl.kind, x, wt, wl.stride, wl.pad, wl.dil)
+    assert err(to_np(out), ref) <= TOL_BF16
+    if integer:
+        # integer partials of 16 channels of {-3..3} products stay below 256: exact in bf16
+        assert np.array_equal(to_np(out), ref)
+    kind, n, c, h, w, k, r, s, st, pd, dl, op = SMALL[1]
+    x = synth.random_tensor((n, h, w, c), 8200, integer=integer)
+    wt = synth.random_tensor((r, s, k, c), 8201, integer=integer)
+    out = run_conv(kind, x, wt, st, pd, dl, op, y_bf16=True)
+    assert err(to_np(out), oracle_conv(kind, x, wt, st, pd, dl, op)) <= TOL_BF16
 
 
 @pytest.mark.parametrize("transposed", [False, True])
@@ -444,10 +497,10 @@ def band_rows_sample(b, l, dil, w, n_random, seed):
 
 
 def check_band(q, k, v, w, dil, scale, mask, staged, rows=None, tol=TOL_BF16,
-               out_dtype=torch.float32):
+               out_dtype=torch.float32, flags=0):
     qg, kg, vg = q.to(DEV), k.to(DEV), v.to(DEV)
     o = ol.banded_bmm(qg, kg, vg, w, dil, scale, mask_invalid=mask, staged=staged,
-                      out_dtype=out_dtype)
+                      out_dtype=out_dtype, flags=flags)
     torch.cuda.synchronize()
     on = to_np(o).reshape(-1, q.shape[2])
     assert np.isfinite(on).all()
@@ -475,31 +528,33 @@ BAND_SMALL = [  # (b, l, w, dil)
 @pytest.mark.parametrize("ci", range(len(BAND_SMALL)))
 @pytest.mark.parametrize("mask", [False, True])
 @pytest.mark.parametrize("staged", [False, True])
-def test_band_small(ci, mask, staged):
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_band_small(ci, mask, staged, out_dtype):
+    """Every path (fused / staged, zero / mask mode) with an fp32 and a bf16 O."""
     b, l, w, dil = BAND_SMALL[ci]
-    say("band small", BAND_SMALL[ci], "mask", mask, "staged", staged)
+    say("band small", BAND_SMALL[ci], "mask", mask, "staged", staged, "O", out_dtype)
     q = synth.random_tensor((b, l, 64), 11000 + ci, "bf16", dist="normal")
     k = synth.random_tensor((b, l, 64), 12000 + ci, "bf16", dist="normal")
     v = synth.random_tensor((b, l, 64), 13000 + ci, "bf16", dist="normal")
-    check_band(q, k, v, w, dil, 0.125, mask, staged)
+    o = check_band(q, k, v, w, dil, 0.125, mask, staged, out_dtype=out_dtype)
+    assert o.dtype == out_dtype
 
 
-# Every wave shape of the fused band kernel (OLLIE_BAND_CONFIG 0-2, read per call): 32
+# Every wave shape of the fused band kernel (flag bits BAND_SHAPE(0..2)): 32
 # or 64 queries per wave, four or two waves per workgroup, on the small cases and
 # sequences long enough for several workgroups per residue subsequence (in the last,
 # the second tile of every odd residue lies past its subsequence).
 @pytest.mark.parametrize("ci", range(len(BAND_SMALL) + 4))
 @pytest.mark.parametrize("mask", [False, True])
 @pytest.mark.parametrize("cfg", [0, 1, 2])
-def test_band_every_wave_shape(cfg, mask, ci, monkeypatch):
+def test_band_every_wave_shape(cfg, mask, ci):
     extra = [(2, 1100, 96, 2), (48, 2000, 64, 3), (64, 2600, 40, 1), (300, 257, 16, 2)]
     b, l, w, dil = BAND_SMALL[ci] if ci < len(BAND_SMALL) else extra[ci - len(BAND_SMALL)]
     say("band wave shape", cfg, (b, l, w, dil), "mask", mask)
-    monkeypatch.setenv("OLLIE_BAND_CONFIG", str(cfg))
     q = synth.random_tensor((b, l, 64), 14000 + ci, "bf16", dist="normal")
     k = synth.random_tensor((b, l, 64), 14100 + ci, "bf16", dist="normal")
     v = synth.random_tensor((b, l, 64), 14200 + ci, "bf16", dist="normal")
-    check_band(q, k, v, w, dil, 0.125, mask, False)
+    check_band(q, k, v, w, dil, 0.125, mask, False, flags=ol.BAND_SHAPE(cfg))
 
 
 @pytest.mark.parametrize("mask", [False, True])
@@ -524,13 +579,27 @@ def test_band_scores_exact_on_integers(mask):
     assert err(pn, pref) <= TOL_BF16
 
 
-@pytest.mark.parametrize("staged", [False, True])
-def test_band_workload(staged):
+_BAND_WL_REF = {}
+
+
+@pytest.mark.parametrize("staged,out_dtype", [(False, torch.float32), (True, torch.float32),
+                                               (False, torch.bfloat16), (True, torch.bfloat16)])
+def test_band_workload_every_row(staged, out_dtype):
+    """The Longformer band workload (zero mode) against the oracle on all 393,216 rows,
+    fused and staged, with an fp32 and a bf16 O (one oracle pass serves the four)."""
     wl = synth.WORKLOADS[5]
-    say("band workload staged", staged)
+    say("band workload, every row, staged", staged, "O", out_dtype)
     q, k, v = synth.band_inputs(wl)
-    rows = band_rows_sample(wl.b, wl.l, wl.dilation, wl.w, 3000, 5)
-    check_band(q, k, v, wl.w, wl.dilation, wl.scale, wl.mask_invalid, staged, rows)
+    if "o" not in _BAND_WL_REF:
+        _BAND_WL_REF["o"] = oracle.band(q, k, v, wl.w, wl.dilation, wl.scale, wl.mask_invalid,
+                                        want_s=False, want_p=False)[2]
+    o = ol.banded_bmm(q.to(DEV), k.to(DEV), v.to(DEV), wl.w, wl.dilation, wl.scale,
+                      mask_invalid=wl.mask_invalid, staged=staged, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    assert o.dtype == out_dtype
+    e = err(to_np(o), _BAND_WL_REF["o"])
+    say("band err %.3e" % e)
+    assert e <= TOL_BF16
 
 
 def test_band_workload_mask_mode_bf16_out():
@@ -668,7 +737,7 @@ def test_small_shapes_fused(ci, integer):
         assert err(to_np(out), ref) <= TOL_BF16
 
 
-# Every tile shape of the fused expression (OLLIE_FUSED_CONFIG 0-12, read per call), on
+# Every tile shape of the fused expression (flag bits FUSED_TILE(0..14)), on
 # shapes that exercise the row-window kernel (config 9: stride-1 forms whose class width
 # is a multiple of 16 dividing 192 -- ragged channel tiles, tiles straddling images,
 # kernel widths 1-3) and on shapes where config 9 falls back to the automatic choice.
@@ -688,19 +757,19 @@ FUSED_CONFIGS = 15
 
 @pytest.mark.parametrize("ci", range(len(TILE_CASES)))
 @pytest.mark.parametrize("cfg", range(FUSED_CONFIGS))
-def test_every_tile_shape_integer_exact(cfg, ci, monkeypatch):
+def test_every_tile_shape_integer_exact(cfg, ci):
     kind, n, c, h, w, k, r, s, st, pd, dl, op, res = TILE_CASES[ci]
     say("tile shape", cfg, TILE_CASES[ci])
-    monkeypatch.setenv("OLLIE_FUSED_CONFIG", str(cfg))
+    fl = ol.FUSED_TILE(cfg)
     x = synth.random_tensor((n, h, w, c), 36000 + ci, "bf16", integer=True)
     wt = synth.random_tensor((r, s, k, c), 36100 + ci, "bf16", integer=True)
     xg, wg = x.to(DEV), wt.to(DEV)
     if kind == "conv2d":
-        out = ol.derived_conv2d(xg, wg, st, pd, fuse=True)
+        out = ol.derived_conv2d(xg, wg, st, pd, fuse=True, flags=fl)
     elif kind == "dilated_conv2d":
-        out = ol.derived_dilated_conv2d(xg, wg, st, pd, dl, fuse=True, residues=res)
+        out = ol.derived_dilated_conv2d(xg, wg, st, pd, dl, fuse=True, residues=res, flags=fl)
     else:
-        out = ol.derived_conv_transpose2d(xg, wg, st, pd, op, dl, fuse=True)
+        out = ol.derived_conv_transpose2d(xg, wg, st, pd, op, dl, fuse=True, flags=fl)
     torch.cuda.synchronize()
     assert np.array_equal(to_np(out), oracle_conv(kind, x, wt, st, pd, dl, op))
 
