@@ -219,6 +219,24 @@ const char* ollie_version(void);
 int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                    void* ws, size_t ws_bytes, uint32_t flags, void* stream);
 
+/* derived_conv2d for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same operator,
+ * arguments and flags as derived_conv2d, with the workspace taken from the library's
+ * own static device array instead of a caller buffer.  The call allocates nothing (no
+ * hipMalloc, hipFree or allocating library routine); x, wt and out are still the
+ * caller's.
+ *   Limit: ollie_conv_workspace_bytes(desc, 0, flags) <= 64 MiB (67108864 bytes), else
+ *   OLLIE_EWORKSPACE and nothing is enqueued.  (The fused path needs no workspace.)
+ *   The array is one per GPU (64 MiB held on every GPU the library runs on, until the
+ *   process ends), shared by every call on that GPU and left holding the last call's
+ *   partials; no kernel reads a byte of it that the same call has not written first.
+ *   Calls on one GPU whose executions overlap (other streams, other threads) race on
+ *   it: serialise them.
+ *   The first call on a device looks up the array's device address once
+ *   (hipGetSymbolAddress; a failure gives OLLIE_EHIP). */
+int ollie_derived_conv2d_noalloc(const ollie_conv_desc* desc, const void* x, const void* wt,
+                                 void* out, uint32_t flags, void* stream);
+
 /* Dilated convolution as the same GEMM plus the dilated OffsetAdd: taps are spaced by
  * the dilation, hi = ho*stride_h - pad_h + r*dil_h, wi = wo*stride_w - pad_w + s*dil_w;
  * taps outside the image read the zero padding and are skipped (boundary tightening,

@@ -58,7 +58,8 @@ EXPORTS = ("derived_conv2d", "derived_dilated_conv2d", "derived_conv_transpose2d
            "ollie_derived_conv_transpose2d_ex",
            "ollie_conv_out_hw", "ollie_conv_workspace_bytes", "ollie_band_workspace_bytes",
            "ollie_last_error", "ollie_version", "ollie_gemm_nt", "ollie_eop_offset_sum",
-           "ollie_eop_convt_gather", "ollie_band_g2bmm", "ollie_band_softmax", "ollie_band_gbmm")
+           "ollie_eop_convt_gather", "ollie_band_g2bmm", "ollie_band_softmax", "ollie_band_gbmm",
+           "ollie_derived_conv2d_noalloc")
 
 
 class ConvDesc(ctypes.Structure):
@@ -115,6 +116,7 @@ def load_library(path: str = LIB_PATH):
         "ollie_derived_dilated_conv2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
         "ollie_derived_conv_transpose2d_ex": ([cdp, p, p, p, p, sz, u32, edp, p], ctypes.c_int),
         "banded_bmm": ([bdp, p, p, p, p, p, p, sz, u32, p], ctypes.c_int),
+        "ollie_derived_conv2d_noalloc": ([cdp, p, p, p, u32, p], ctypes.c_int),
         "ollie_conv_out_hw": ([cdp, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64)],
                               ctypes.c_int),
         "ollie_conv_workspace_bytes": ([cdp, ctypes.c_int, u32], sz),
@@ -262,6 +264,34 @@ def derived_conv2d(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=F
     return _conv("derived_conv2d", False, x, wt, stride, padding, 1, 0, out_dtype, y_bf16,
                  out, ws, fuse, bias, residual, relu,
                  (CONV_SPLIT_3X3 if split3x3 else 0) | flags)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def derived_conv2d_noalloc(x, wt, stride=1, padding=0, out_dtype=torch.float32, y_bf16=False,
+                           out=None, fuse=False, split3x3=False, flags=0):
+    """derived_conv2d through ollie_derived_conv2d_noalloc: the workspace is the library's
+    static per-GPU scratch array (at most NOALLOC_SCRATCH_BYTES), so the library call
+    itself allocates nothing.  `out` is allocated here when not given."""
+    _gpu(x, "x")
+    _gpu(wt, "wt")
+    if x.dtype != wt.dtype:
+        raise ValueError("x and wt must have the same dtype")
+    desc = conv_desc(tuple(x.shape), tuple(wt.shape), stride, padding, 1, 0, x.dtype, out_dtype)
+    fl = (Y_BF16 if y_bf16 else 0) | (FUSE_EPILOGUE if fuse else 0) | \
+        (CONV_SPLIT_3X3 if split3x3 else 0) | flags
+    ho, wo = conv_out_hw(desc, False)
+    if out is None:
+        out = torch.empty((desc.n, ho, wo, desc.k), dtype=out_dtype, device=x.device)
+    else:
+        _gpu(out, "out")
+        if tuple(out.shape) != (desc.n, ho, wo, desc.k) or out.dtype != out_dtype:
+            raise ValueError("out has the wrong shape or dtype")
+    st = load_library().ollie_derived_conv2d_noalloc(ctypes.byref(desc), _ptr(x), _ptr(wt),
+                                                     _ptr(out), fl, _stream(x.device))
+    _check(st, "ollie_derived_conv2d_noalloc")
+    return out
 
 
 def derived_dilated_conv2d(x, wt, stride=1, padding=0, dilation=1, out_dtype=torch.float32,

@@ -5,6 +5,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "../../include/ollie.h"
 #include "common.h"
 
@@ -230,16 +232,18 @@ int make_epi(const ollie_conv_epilogue* e, const ollie_conv_desc* d, const void*
     return OLLIE_OK;
 }
 
+// dry = true: every check runs, and the call returns OLLIE_OK right before its first
+// HIP call (nothing is launched, no pointer is dereferenced).
 int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
                 void* out, void* ws, size_t ws_bytes, uint32_t flags,
-                const ollie_conv_epilogue* epilogue, void* stream);
+                const ollie_conv_epilogue* epilogue, void* stream, bool dry = false);
 
 // The R x S -> 3x3 derived form: weight split, the 3x3 stage into Z (fp32), then the
 // OffsetAdd over the kernel blocks (taps spaced 3 apart in Z, shifted by er, es),
 // which carries the element-wise tail.
 int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
                 void* out, void* ws, size_t ws_bytes, uint32_t flags, const Epi& epi,
-                int64_t ho, int64_t wo, void* stream) {
+                int64_t ho, int64_t wo, void* stream, bool dry) {
     const Split3 q = split3_of(d);
     int64_t hz, wz;
     int st = check_split3(d, transposed, q, &hz, &wz);
@@ -263,6 +267,7 @@ int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const v
                         (flags & OLLIE_Y_BF16) ? OLLIE_BF16 : OLLIE_F32);
         if (st) return st;
     }
+    if (dry) return OLLIE_OK;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = launch_split_weights_3x3(conv_geom(d, ho, wo), wt, w3,
                                             d->in_dtype == OLLIE_BF16, s);
@@ -286,7 +291,7 @@ int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const v
 
 int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
                 void* out, void* ws, size_t ws_bytes, uint32_t flags,
-                const ollie_conv_epilogue* epilogue, void* stream) {
+                const ollie_conv_epilogue* epilogue, void* stream, bool dry) {
     int64_t ho, wo;
     int st = check_conv_geom(d, transposed, &ho, &wo);
     if (st) return st;
@@ -322,7 +327,7 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
             return fail(OLLIE_EINVAL, "OLLIE_CONV_SPLIT_3X3 and OLLIE_DILATED_RESIDUES exclude "
                                       "each other");
         return conv_split3(d, transposed, x, wt, out, ws, ws_bytes,
-                           flags & ~(uint32_t)OLLIE_CONV_SPLIT_3X3, epi, ho, wo, stream);
+                           flags & ~(uint32_t)OLLIE_CONV_SPLIT_3X3, epi, ho, wo, stream, dry);
     }
     if ((flags & OLLIE_DILATED_RESIDUES) && !fused_path(d, transposed, ho, wo, flags))
         return fail(OLLIE_EINVAL,
@@ -331,6 +336,7 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     if (fused_path(d, transposed, ho, wo, flags)) {
         if (!aligned16(x) || !aligned16(wt) || !aligned16(out))
             return fail(OLLIE_EALIGN, "tensor pointers must be 16-byte aligned");
+        if (dry) return OLLIE_OK;
         hipError_t e = launch_conv_fused(conv_geom(d, ho, wo), conv_form(transposed, flags), x,
                                          wt, out, d->out_dtype == OLLIE_BF16, epi,
                                          fused_tile(flags), (hipStream_t)stream);
@@ -348,6 +354,7 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
     st = check_gemm(m, nc, d->c, x, wt, ws, d->in_dtype,
                     (flags & OLLIE_Y_BF16) ? OLLIE_BF16 : OLLIE_F32);
     if (st) return st;
+    if (dry) return OLLIE_OK;
     hipStream_t s = (hipStream_t)stream;
     const int y_bf16 = (flags & OLLIE_Y_BF16) ? 1 : 0;
     hipError_t e = launch_gemm_nt(m, nc, d->c, x, wt, ws, d->in_dtype == OLLIE_BF16, y_bf16,
@@ -396,6 +403,53 @@ size_t band_qkv_bytes(const ollie_band_desc* d) { return (size_t)(d->b * d->l * 
 
 constexpr int64_t kSoftmaxMaxBand = 16 * 64;   // register-resident row length of the staged softmax
 
+// derived_conv2d with an optional element-wise tail (the exported _ex entry point and
+// the allocation-free variant both end here).
+int derived_conv2d_ex_impl(const ollie_conv_desc* desc, const void* x, const void* wt,
+                           void* out, void* ws, size_t ws_bytes, uint32_t flags,
+                           const ollie_conv_epilogue* epi, void* stream, bool dry = false) {
+    if (flags & OLLIE_DILATED_RESIDUES)
+        return fail(OLLIE_EINVAL, "OLLIE_DILATED_RESIDUES applies to derived_dilated_conv2d");
+    if (desc && (desc->dil_h != 1 || desc->dil_w != 1))
+        return fail(OLLIE_EINVAL, "derived_conv2d takes dilation 1; use derived_dilated_conv2d");
+    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream, dry);
+}
+
+}  // namespace
+
+// The library's own workspace for callers that cannot allocate (ollie_derived_conv2d_
+// noalloc): a file-scope device array, one copy per GPU, alive until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: kernels and
+// copies get the device address that hipGetSymbolAddress returns for the current
+// device, looked up on the first such call on that device and kept per device.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array, or an OLLIE_EHIP status.
+int scratch_ptr(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(OLLIE_EINVAL, "device index %d beyond the %d the scratch table holds", dev,
+                    kMaxDevices);
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        // idempotent: racing first calls on one device store the same address
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(OLLIE_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return OLLIE_OK;
+}
+
 }  // namespace
 
 #pragma GCC visibility push(default)
@@ -428,11 +482,7 @@ int ollie_derived_conv2d_ex(const ollie_conv_desc* desc, const void* x, const vo
                       void* ws, size_t ws_bytes, uint32_t flags,
                       const ollie_conv_epilogue* epi, void* stream) {
     g_err[0] = 0;
-    if (flags & OLLIE_DILATED_RESIDUES)
-        return fail(OLLIE_EINVAL, "OLLIE_DILATED_RESIDUES applies to derived_dilated_conv2d");
-    if (desc && (desc->dil_h != 1 || desc->dil_w != 1))
-        return fail(OLLIE_EINVAL, "derived_conv2d takes dilation 1; use derived_dilated_conv2d");
-    return conv_common(desc, 0, x, wt, out, ws, ws_bytes, flags, epi, stream);
+    return derived_conv2d_ex_impl(desc, x, wt, out, ws, ws_bytes, flags, epi, stream);
 }
 
 int ollie_derived_dilated_conv2d_ex(const ollie_conv_desc* desc, const void* x, const void* wt,
@@ -456,6 +506,34 @@ int ollie_derived_conv_transpose2d_ex(const ollie_conv_desc* desc, const void* x
 int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                    void* ws, size_t ws_bytes, uint32_t flags, void* stream) {
     return ollie_derived_conv2d_ex(desc, x, wt, out, ws, ws_bytes, flags, nullptr, stream);
+}
+
+int ollie_derived_conv2d_noalloc(const ollie_conv_desc* desc, const void* x, const void* wt,
+                                 void* out, uint32_t flags, void* stream) {
+    g_err[0] = 0;
+    int64_t ho, wo;
+    int st = check_conv_geom(desc, 0, &ho, &wo);
+    if (st) return st;
+    const size_t need = ollie_conv_workspace_bytes(desc, 0, flags);
+    if (need > kScratchBytes)
+        return fail(OLLIE_EWORKSPACE,
+                    "needs %zu bytes of workspace; the static scratch holds %zu (use "
+                    "derived_conv2d with a caller workspace)", need, kScratchBytes);
+    // Every argument check first, without a HIP call: a dry run of the same path whose
+    // workspace is a placeholder range at 2^63 (the kernel half of the address space,
+    // which no caller buffer can occupy, so the overlap checks see the scratch as what
+    // it is: disjoint from the caller's tensors).  Nothing is dereferenced or launched.
+    void* const placeholder = reinterpret_cast<void*>(uintptr_t(1) << 63);
+    st = derived_conv2d_ex_impl(desc, x, wt, out, need ? placeholder : nullptr,
+                                need ? kScratchBytes : 0, flags, nullptr, stream, true);
+    if (st) return st;
+    void* ws = nullptr;
+    if (need) {
+        st = scratch_ptr(&ws);
+        if (st) return st;
+    }
+    return derived_conv2d_ex_impl(desc, x, wt, out, ws, need ? kScratchBytes : 0, flags,
+                                  nullptr, stream);
 }
 
 int derived_dilated_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt,

@@ -420,3 +420,19 @@ def test_stale_library_is_rebuilt(tmp_path, monkeypatch):
     monkeypatch.setattr(_build, "build", lambda *a, **k: calls.append(1) or _build.LIB)
     ol.load_library()
     assert calls == [1]
+
+
+def test_noalloc_entry_rejects_oversized_and_invalid_calls(lib):
+    """ollie_derived_conv2d_noalloc: a workspace beyond its 64 MiB static scratch gives
+    OLLIE_EWORKSPACE, invalid descriptors the usual status, all before any HIP call."""
+    def call(d, flags=0):
+        st = lib.ollie_derived_conv2d_noalloc(ctypes.byref(d) if d is not None else None,
+                                              A16, B16, C16, flags, None)
+        return st, lib.ollie_last_error().decode()
+    big = conv(n=1, c=512, h=96, w=128, k=512, pad=2)          # 226 MB fp32 scope
+    st, msg = call(big)
+    assert st == ol.EWORKSPACE and "scratch" in msg
+    assert call(None)[0] == ol.EINVAL
+    assert call(conv(stride=0))[0] == ol.EINVAL
+    assert call(conv(dil=2, pad=2))[0] == ol.EINVAL             # dilation belongs elsewhere
+    assert call(conv(in_dtype=7))[0] == ol.EDTYPE
