@@ -13,24 +13,30 @@ both variants are timed and reported.
 the step time).  Per workload it also reports the GEMM stage in TFLOP/s and % of the
 bf16 MFMA peak (and, since its fp32 Y makes it HBM-bound on these shapes, its HBM
 GB/s and % of the roofline that binds it; the same stage with a bf16 Y appears warm as
-gemm_ybf16_*), the eOperator stage in GB/s and % of the HBM peak, and the fused kernel
-in TFLOP/s, each measured two ways:
+gemm_ybf16_*), the eOperator stage in GB/s and % of the HBM peak, the fused kernel in
+TFLOP/s, and for the band also the three stages of its staged form (G2BMM, softmax
+eOperator, GBMM) in GB/s and % of the HBM peak, each measured two ways:
   warm     HIP events around a HIP graph of back-to-back launches of that kernel (host
-           launch gaps do not count), on the stream it runs on;
-  cold     ("cold" block) the median of single launches, each bracketed by HIP events
-           after a 512 MB buffer read that evicts L2 and the MALL.
+           launch gaps do not count), on the stream it runs on.  Operands and the staged
+           scope stay in the 256 MB MALL between such launches, so warm eOperator rates
+           are MALL-assisted (named *_mall_assisted), not HBM fractions;
+  cold     ("cold" block, the reference figures) the kernel's duration after a 512 MB
+           read that evicts L2 and the MALL, from HIP graphs of 20 (flush, kernel),
+           (flush, fill) and (flush, fill, fill) sequences (fill: a one-element fill),
+           combined so that the flush, the fill and the event overhead cancel.
 `roofline` covers the kernel with the largest share of a step (warm; frac_cold from the
-cold median).
+cold duration).
 
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workloads.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
-       python bench.py --stage NAME [--steps K]   (launch one stage kernel K times, for
-       profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg>, fused:<cfg> for cfg 2-4, fusedres:4
-       (the dilated workload as residue sub-image convolutions), band_fused,
-       band_g2bmm, band_softmax, band_gbmm, srcnn_direct_fused, srcnn_split3x3,
-       srcnn_direct_staged (the SRCNN conv5x5 workload), or copy = a plain 256 MiB
-       device copy)
+       python bench.py --stage NAME [--steps K] [--cold]   (launch one stage kernel K
+       times, for profiling; NAME is gemm:<cfg>, eop:<cfg>, op:<cfg>, fused:<cfg> for cfg
+       2-4, fusedres:4 (the dilated workload as residue sub-image convolutions),
+       band_fused, band_g2bmm, band_softmax, band_gbmm, srcnn_direct_fused,
+       srcnn_split3x3, srcnn_split3x3_chain, srcnn_direct_staged (the SRCNN conv5x5
+       workload), or copy = a plain 256 MiB device copy; --cold puts a 512 MB read
+       before every launch)
 """
 from __future__ import annotations
 
@@ -119,11 +125,16 @@ def srcnn_calls(dev):
         return torch.empty(max(ol.conv_workspace_bytes(desc, False, flags), 16),
                            dtype=torch.uint8, device=dev)
     ws_split = ws(ol.CONV_SPLIT_3X3 | ol.FUSE_EPILOGUE)
+    ws_chain = ws(ol.CONV_SPLIT_3X3)
     ws_staged = ws(0)
     fns = {
         "direct_fused": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out, fuse=True),
         "split3x3": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out, ws=ws_split,
                                               fuse=True, split3x3=True),
+        # the split form through the 3x3 stage's GEMM and its two eOperators fused into
+        # one kernel (the intermediate Z is never formed)
+        "split3x3_chain": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out,
+                                                    ws=ws_chain, split3x3=True),
         "direct_staged": lambda: ol.derived_conv2d(x, wt, wl.stride, wl.pad, out=out,
                                                    ws=ws_staged),
     }
@@ -141,6 +152,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--stage", default=None, help="launch only this stage kernel")
+    ap.add_argument("--cold", action="store_true",
+                    help="with --stage: a 512 MB read before every launch (cold caches)")
     ap.add_argument("--streams", type=int, default=1, choices=[1, 2, 4],
                     help="streams the step's independent operators are spread over: 1 = "
                          "all in order on one stream, 2 = the band beside the three "
@@ -302,12 +315,52 @@ def main():
         d = sorted(a.elapsed_time(b) for a, b in evs)
         return d[len(d) // 2] if len(d) % 2 else 0.5 * (d[len(d) // 2 - 1] + d[len(d) // 2])
 
+    # Cold kernel durations without the launch and event overhead, from HIP graphs of
+    # `reps` repetitions replayed three times between events (medians):
+    #   A = (flush, kernel),  C = (flush, fill),  D = (flush, fill, fill)
+    # with `fill` a one-element fill.  Per repetition A - C = kernel - fill and
+    # D - C = fill + one launch gap, so (A + D - 2C) / reps is the kernel's duration
+    # after a flush (plus one gap between graph nodes): the flush, the fill and the
+    # event overhead cancel.  Cross-checked against rocprofv3 kernel traces of the same
+    # pairs (bench.py --stage NAME --cold).
+    noop = lambda: flush_sink.fill_(0.0)
+
+    def seq_graph_ms(seq, reps):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                for f in seq:
+                    f()
+        g.replay()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(3):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1))
+        del g
+        return sorted(times)[1]
+
+    flush_fn = lambda: torch.amax(flush, dim=0, out=flush_sink)
     reps = max(args.steps, 10)
     reps_cold = max(args.steps, 30)
+    reps_pair = 20
+    base_c_ms = seq_graph_ms([flush_fn, noop], reps_pair)
+    base_d_ms = seq_graph_ms([flush_fn, noop, noop], reps_pair)
+
+    def time_kernel_cold_dur(fn):
+        fn()
+        torch.cuda.synchronize()
+        a_ms = seq_graph_ms([flush_fn, fn], reps_pair)
+        return max((a_ms + base_d_ms - 2 * base_c_ms) / reps_pair, 0.0)
+
     # what a single launch costs between its events on this stream: a one-element fill,
-    # timed like the cold launches (part of every cold figure, most visible on the
-    # few-microsecond kernels)
-    event_floor = time_kernel_cold(lambda: flush_sink.fill_(0.0), reps_cold)
+    # timed like the event-bracketed cold launches (part of each such figure)
+    event_floor = time_kernel_cold(noop, reps_cold)
     per_cfg = {}
     kernels = []   # (name, ms per launch, bound, achieved, peak, unit, algorithmic work)
     for op in conv_ops:
@@ -325,9 +378,10 @@ def main():
         gb_ms = time_kernel(lambda: ol.gemm_nt(a, b, y_dtype=torch.bfloat16, out=yb), reps)
         e_ms = time_kernel(e_fn, reps)
         f_ms = time_kernel(f_fn, reps)
-        g_cold = time_kernel_cold(g_fn, reps_cold)
-        e_cold = time_kernel_cold(e_fn, reps_cold)
-        f_cold = time_kernel_cold(f_fn, reps_cold)
+        g_cold = time_kernel_cold_dur(g_fn)
+        e_cold = time_kernel_cold_dur(e_fn)
+        f_cold = time_kernel_cold_dur(f_fn)
+        e_cold_ev = time_kernel_cold(e_fn, reps_cold)
         r_ms = None
         if op["cfg"] == 4:   # the dilated workload also in the residue sub-image form
             r_ms = time_kernel(lambda: op["entry"](op["x"], op["wt"],
@@ -356,8 +410,8 @@ def main():
             "gemm_ybf16_ms": round(gb_ms, 5),
             "gemm_ybf16_tflops": round(op["flops"] / (gb_ms * 1e-3) / 1e12, 2),
             "gemm_ybf16_pct_mfma_peak": round(100 * t_mfma / (gb_ms * 1e-3), 2),
-            "eop_ms": round(e_ms, 5), "eop_gbs": round(e_gb, 1),
-            "eop_pct_hbm_peak": round(100 * e_gb / PEAK_HBM_GBS, 2),
+            "eop_ms": round(e_ms, 5), "eop_gbs_mall_assisted": round(e_gb, 1),
+            "eop_pct_hbm_peak_mall_assisted": round(100 * e_gb / PEAK_HBM_GBS, 2),
             "fused_ms": round(f_ms, 5), "fused_tflops": round(f_tf, 2),
             "fused_pct_mfma_peak": round(100 * f_tf / PEAK_BF16_TFLOPS, 2),
             "gemm_gflop": round(op["flops"] / 1e9, 4), "gemm_mbytes": round(g_bytes / 1e6, 3),
@@ -373,6 +427,7 @@ def main():
                      "eop_gbs": round(op["eop_bytes"] / (e_cold * 1e-3) / 1e9, 1),
                      "eop_pct_hbm_peak": round(100 * op["eop_bytes"] / (e_cold * 1e-3)
                                                / (PEAK_HBM_GBS * 1e9), 2),
+                     "eop_event_bracketed_ms": round(e_cold_ev, 5),
                      "fused_ms": round(f_cold, 5),
                      "fused_tflops": round(op["flops"] / (f_cold * 1e-3) / 1e12, 2),
                      "fused_pct_mfma_peak": round(100 * t_mfma / (f_cold * 1e-3), 2)},
@@ -392,7 +447,7 @@ def main():
             kernels.append((f"eop_gather[{name}]", e_ms, "hbm", e_gb, PEAK_HBM_GBS, "GB/s",
                             op["eop_bytes"]))
     b_ms = time_kernel(band_call, reps)
-    b_cold = time_kernel_cold(band_call, reps_cold)
+    b_cold = time_kernel_cold_dur(band_call)
     b_tf = bflops / (b_ms * 1e-3) / 1e12
     per_cfg[bwl.name] = {"path": "fused", "op_ms": round(b_ms, 5), "fused_ms": round(b_ms, 5),
                          "band_tflops": round(b_tf, 2),
@@ -403,6 +458,38 @@ def main():
                                   "band_pct_mfma_peak": round(
                                       100 * bflops / (b_cold * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                       2)}}
+    # the staged band (OLLIE_BAND_STAGED): G2BMM -> softmax eOperator -> GBMM through S
+    # (fp32) and P (bf16), each an HBM-bound stage with algorithmic bytes
+    #   G2BMM: Q + K read, S written;  softmax: S read, P written;  GBMM: P + V read, O written
+    nbnd = 2 * bwl.w + 1
+    rows = bwl.b * bwl.l
+    s_st = torch.empty((bwl.b, bwl.l, nbnd), dtype=torch.float32, device=dev)
+    p_st = torch.empty((bwl.b, bwl.l, nbnd), dtype=torch.bfloat16, device=dev)
+    ol.band_g2bmm(q, k, bwl.w, bwl.dilation, bwl.scale, s=s_st)
+    ol.band_softmax(s_st, bwl.w, bwl.dilation, bwl.mask_invalid, p=p_st)
+    qkv_bytes = rows * bwl.d * 2
+    stages = {
+        "g2bmm": (lambda: ol.band_g2bmm(q, k, bwl.w, bwl.dilation, bwl.scale, s=s_st),
+                  2 * qkv_bytes + rows * nbnd * 4),
+        "softmax_eop": (lambda: ol.band_softmax(s_st, bwl.w, bwl.dilation, bwl.mask_invalid,
+                                                p=p_st), rows * nbnd * (4 + 2)),
+        "gbmm": (lambda: ol.band_gbmm(p_st, v, bwl.w, bwl.dilation, o=o),
+                 rows * nbnd * 2 + qkv_bytes + rows * bwl.d * 4),
+    }
+    staged = {}
+    for nm, (fn, nbytes) in stages.items():
+        w_ms = time_kernel(fn, reps)
+        c_ms = time_kernel_cold_dur(fn)
+        staged[nm] = {"warm_ms": round(w_ms, 5), "cold_ms": round(c_ms, 5),
+                      "mbytes": round(nbytes / 1e6, 2),
+                      "gbs": round(nbytes / (c_ms * 1e-3) / 1e9, 1),
+                      "pct_hbm_peak": round(100 * nbytes / (c_ms * 1e-3) / (PEAK_HBM_GBS * 1e9),
+                                            2)}
+    staged["op_ms"] = round(sum(staged[n]["warm_ms"] for n in stages), 5)
+    per_cfg[bwl.name]["staged"] = staged
+    per_cfg[bwl.name]["eop_ms"] = staged["softmax_eop"]["cold_ms"]
+    per_cfg[bwl.name]["eop_pct_hbm_peak"] = staged["softmax_eop"]["pct_hbm_peak"]
+    del s_st, p_st
     kernels.append((f"band_fused[{bwl.name}]", b_ms, "mfma", b_tf, PEAK_BF16_TFLOPS, "TFLOP/s",
                     bflops))
     # ------------------------- the Conv5x5 -> Conv3x3 derived form (a workload of its own,
@@ -417,7 +504,7 @@ def main():
                                           / (swl.r * swl.s), 4)}
     for nm, fn in s_fns.items():
         w_ms = time_kernel(fn, reps)
-        c_ms = time_kernel_cold(fn, reps_cold)
+        c_ms = time_kernel_cold_dur(fn)
         row[f"{nm}_ms"] = round(w_ms, 5)
         row[f"{nm}_tflops"] = round(s_flops / (w_ms * 1e-3) / 1e12, 2)
         row[f"{nm}_cold_ms"] = round(c_ms, 5)
@@ -496,7 +583,8 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
             fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], fuse=True))
         elif kind == "fusedres":
             fn = lambda: op["entry"](op["x"], op["wt"], **dict(op["kw"], ws=None, residues=True))
-    elif name in ("srcnn_direct_fused", "srcnn_split3x3", "srcnn_direct_staged"):
+    elif name in ("srcnn_direct_fused", "srcnn_split3x3", "srcnn_split3x3_chain",
+                  "srcnn_direct_staged"):
         fn = srcnn_calls(q.device)[1][name[len("srcnn_"):]]
     elif name == "band_fused":
         fn = lambda: ol.banded_bmm(q, k, v, bwl.w, bwl.dilation, bwl.scale,
@@ -519,10 +607,17 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
         fn()
     torch.cuda.synchronize()
     # a HIP graph of `steps` launches, replayed between two events: kernel time only,
-    # no host launch gaps (the same method as the main benchmark's per-kernel figures)
+    # no host launch gaps (the same method as the main benchmark's per-kernel figures);
+    # with --cold each launch follows a 512 MB read that evicts L2 and the MALL (the
+    # pairs of the benchmark's cold figures, so a kernel trace of this run gives the
+    # cold kernel durations directly)
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=q.device) if args.cold else None
+    sink = torch.empty((), dtype=torch.float32, device=q.device)
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         for _ in range(args.steps):
+            if flush is not None:
+                torch.amax(flush, dim=0, out=sink)
             fn()
     graph.replay()
     torch.cuda.synchronize()
@@ -532,8 +627,9 @@ def run_stage(args, conv_ops, bwl, q, k, v, o, stream):
     graph.replay()
     e1.record(stream)
     e1.synchronize()
-    print(json.dumps({"stage": name, "launches": args.steps,
-                      "avg_ms": round(e0.elapsed_time(e1) / args.steps, 5)}), flush=True)
+    print(json.dumps({"stage": name, "launches": args.steps, "cold": bool(args.cold),
+                      "avg_ms_incl_flush" if args.cold else "avg_ms":
+                          round(e0.elapsed_time(e1) / args.steps, 5)}), flush=True)
 
 
 def cpu_baseline(conv_ops, bwl):

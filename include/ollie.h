@@ -210,12 +210,20 @@ const char* ollie_version(void);
  * convolution with padding ph + er, pw + es, so i < h + 2(ph + er) - 2), and the outer
  * sum over the kernel blocks is an OffsetAdd with offset step 3:
  *   out[n][ho][wo][k] = sum_{a < nbr, b < nbs} Z[n][ho + er + 3a][wo + es + 3b][(a*nbs + b)*K + k].
- * Kernels: the weight split, the 3x3 stage (fused with OLLIE_FUSE_EPILOGUE when the
- * fused kernel covers it, else GEMM + OffsetAdd, whose Y honours OLLIE_Y_BF16), the
- * block OffsetAdd (which takes the element-wise tail).  ws holds, each at a 256-byte
- * aligned offset: W3 [3][3][nbr*nbs*K][c] in in_dtype, Z in fp32, then the 3x3
- * stage's scope Y when that stage is not fused.  Needs stride 1 and dilation 1, else
- * OLLIE_EINVAL. */
+ * Kernels: the weight split, then either
+ *   - with OLLIE_FUSE_EPILOGUE where the fused kernel covers the 3x3 stage: that stage
+ *     as the fused kernel into Z, and the block OffsetAdd over Z; or
+ *   - otherwise: the 3x3 stage's GEMM into its scope
+ *     Y[m][(r'*3 + s')*nbr*nbs*K + (a*nbs + b)*K + k] (fp32, or bf16 with OLLIE_Y_BF16),
+ *     and its two consecutive eOperators (the 3x3 OffsetAdd, then the block OffsetAdd)
+ *     fused into one (eOperator fusion, section 5.4):
+ *       out[n][ho][wo][k] = sum_{r<R, s<S} [0 <= hi < h][0 <= wi < w]
+ *           Y[(n*h + hi)*w + wi][((r%3)*3 + s%3)*nbr*nbs*K + ((r/3)*nbs + s/3)*K + k]
+ *       with hi = ho - ph + r, wi = wo - pw + s (the relaxed taps carry zero weights and
+ *       are not read), so Z is never formed.
+ * The last kernel takes the element-wise tail.  ws holds W3 [3][3][nbr*nbs*K][c] in
+ * in_dtype, then (at the next 256-byte aligned offset) Z in fp32 or the scope Y.
+ * Needs stride 1 and dilation 1, else OLLIE_EINVAL. */
 int derived_conv2d(const ollie_conv_desc* desc, const void* x, const void* wt, void* out,
                    void* ws, size_t ws_bytes, uint32_t flags, void* stream);
 

@@ -12,7 +12,9 @@ module evaluates the *derived* expression the method reaches, in float64 NumPy:
   is relaxed to whole 3x3 blocks with zero weights (boundary relaxing), the tap index
   substituted as r = 3a + r' (variable substitution), and the sum split into an inner
   3x3 convolution over (r', s', c) with one output-channel group per block (a, b) and
-  an outer OffsetAdd over the blocks with offset step 3 (summation splitting);
+  an outer OffsetAdd over the blocks with offset step 3 (summation splitting); and the
+  same form with its two consecutive eOperators fused into one over the 3x3 stage's
+  scope (eOperator fusion, section 5.4), which never forms the intermediate Z;
 * banded matmul: the dilated band is split by residue i mod dil into non-dilated
   bands over strided subsequences (the dilated-to-non-dilated G2BMM rewrite of
   section 6.4), each evaluated with dense matrix products, then re-interleaved.
@@ -140,6 +142,42 @@ def derived_conv2d_split3x3(x, wt, pad):
             g = a * nbs + b
             out += z[:, er + 3 * a:er + 3 * a + ho_n, es + 3 * b:es + 3 * b + wo_n,
                      g * k:(g + 1) * k]
+    return out
+
+
+def derived_conv2d_split3x3_chain(x, wt, pad):
+    """The 3x3 derived form with its two consecutive eOperators fused into one
+    (eOperator fusion, section 5.4).  The inner 3x3 stage's scope is
+        Y[m, (r'*3 + s')*nbr*nbs*K + (a*nbs + b)*K + k]   (GEMM with the split weights);
+    its OffsetAdd (padding pad + er, taps r', s') substituted into the block OffsetAdd
+    (offset step 3, shift er) gives one eOperator over Y,
+        out[n, ho, wo, k] = sum_{a, b, r', s'} Y[(n, hi, wi), ((r'*3 + s')*nbr*nbs + a*nbs + b)*K + k]
+    with hi = ho + er + 3a - (ph + er) + r' = ho - ph + 3a + r' (likewise wi), over the
+    input pixels inside the image.  Every tap of the relaxed 3*nbr x 3*nbs kernel is
+    summed here (the relaxed ones read partials of zero weights); Z is never formed."""
+    n_, h, w, _ = x.shape
+    r_n, s_n, k, _ = wt.shape
+    ph, pw = pad
+    nbr, nbs = -(-r_n // 3), -(-s_n // 3)
+    w3 = split_weights_3x3(wt)
+    y = gemm_stage(x, w3)                                    # [M, 9 * nbr*nbs*K]
+    y7 = y.reshape(n_, h, w, 3, 3, nbr * nbs, k)
+    ho_n = conv_out_size(h, r_n, 1, ph, 1)
+    wo_n = conv_out_size(w, s_n, 1, pw, 1)
+    out = np.zeros((n_, ho_n, wo_n, k), dtype=np.float64)
+    for a in range(nbr):
+        for b in range(nbs):
+            for rp in range(3):
+                for sp in range(3):
+                    for ho in range(ho_n):
+                        hi = ho - ph + 3 * a + rp
+                        if hi < 0 or hi >= h:
+                            continue
+                        for wo in range(wo_n):
+                            wi = wo - pw + 3 * b + sp
+                            if wi < 0 or wi >= w:
+                                continue
+                            out[:, ho, wo, :] += y7[:, hi, wi, rp, sp, a * nbs + b, :]
     return out
 
 

@@ -167,12 +167,17 @@ int check_split3(const ollie_conv_desc* d, int transposed, const Split3& q, int6
     return OLLIE_OK;
 }
 
+// Workspace of the split form: W3, then either Z (fp32; the 3x3 stage is the fused
+// kernel) or the 3x3 stage's scope Y [n*h*w][9*nbr*nbs*K] (the GEMM stage, whose two
+// eOperators run fused into one and never form Z).
 size_t split3_ws(const ollie_conv_desc* d, const Split3& q, int64_t hz, int64_t wz,
                  uint32_t flags) {
     const size_t el = d->in_dtype == OLLIE_BF16 ? 2 : 4;
     const size_t w3 = (size_t)9 * (size_t)q.d3.k * (size_t)d->c * el;
-    const size_t z = (size_t)(d->n * hz * wz) * (size_t)q.d3.k * 4;
-    return align256(w3) + align256(z) + conv_ws_plain(&q.d3, 0, hz, wz, flags);
+    if (fused_path(&q.d3, 0, hz, wz, flags))
+        return align256(w3) + (size_t)(d->n * hz * wz) * (size_t)q.d3.k * 4;
+    return align256(w3) + (size_t)(d->n * d->h * d->w) * (size_t)(9 * q.d3.k) *
+                              ((flags & OLLIE_Y_BF16) ? 2 : 4);
 }
 
 size_t conv_ws(const ollie_conv_desc* d, int transposed, int64_t ho, int64_t wo,
@@ -238,9 +243,12 @@ int conv_common(const ollie_conv_desc* d, int transposed, const void* x, const v
                 void* out, void* ws, size_t ws_bytes, uint32_t flags,
                 const ollie_conv_epilogue* epilogue, void* stream, bool dry = false);
 
-// The R x S -> 3x3 derived form: weight split, the 3x3 stage into Z (fp32), then the
-// OffsetAdd over the kernel blocks (taps spaced 3 apart in Z, shifted by er, es),
-// which carries the element-wise tail.
+// The R x S -> 3x3 derived form: the weight split, then
+//   * the 3x3 stage as the fused kernel into Z (fp32), and the OffsetAdd over the kernel
+//     blocks (taps spaced 3 apart in Z, shifted by er, es); or
+//   * the 3x3 stage's GEMM into its scope Y, and its OffsetAdd and the block OffsetAdd
+//     fused into one eOperator over Y (Z is never formed);
+// the last kernel carries the element-wise tail.
 int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const void* wt,
                 void* out, void* ws, size_t ws_bytes, uint32_t flags, const Epi& epi,
                 int64_t ho, int64_t wo, void* stream, bool dry) {
@@ -249,7 +257,8 @@ int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const v
     int st = check_split3(d, transposed, q, &hz, &wz);
     if (st) return st;
     const size_t need = split3_ws(d, q, hz, wz, flags);
-    if (!ws) return fail(OLLIE_EINVAL, "null workspace pointer (the split form needs W3 and Z)");
+    if (!ws) return fail(OLLIE_EINVAL, "null workspace pointer (the split form needs W3 and Z "
+                                       "or the 3x3 stage's scope)");
     if (ws_bytes < need)
         return fail(OLLIE_EWORKSPACE, "workspace too small: need %zu bytes, got %zu", need,
                     ws_bytes);
@@ -257,14 +266,15 @@ int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const v
         return fail(OLLIE_EALIGN, "tensor and workspace pointers must be 16-byte aligned");
     const size_t el = d->in_dtype == OLLIE_BF16 ? 2 : 4;
     const size_t w3_bytes = align256((size_t)9 * (size_t)q.d3.k * (size_t)d->c * el);
-    const size_t z_bytes = align256((size_t)(d->n * hz * wz) * (size_t)q.d3.k * 4);
     char* w3 = static_cast<char*>(ws);
-    char* z = w3 + w3_bytes;
-    char* inner = z + z_bytes;
+    char* z = w3 + w3_bytes;   // Z, or the 3x3 stage's scope Y
+    const bool fused3 = fused_path(&q.d3, 0, hz, wz, flags);
+    const int64_t m = d->n * d->h * d->w;
+    const int y_bf16 = (flags & OLLIE_Y_BF16) ? 1 : 0;
     // everything the 3x3 stage checks, before the first launch
-    if (!fused_path(&q.d3, 0, hz, wz, flags)) {
-        st = check_gemm(d->n * d->h * d->w, 9 * q.d3.k, d->c, x, w3, inner, d->in_dtype,
-                        (flags & OLLIE_Y_BF16) ? OLLIE_BF16 : OLLIE_F32);
+    if (!fused3) {
+        st = check_gemm(m, 9 * q.d3.k, d->c, x, w3, z, d->in_dtype,
+                        y_bf16 ? OLLIE_BF16 : OLLIE_F32);
         if (st) return st;
     }
     if (dry) return OLLIE_OK;
@@ -272,8 +282,16 @@ int conv_split3(const ollie_conv_desc* d, int transposed, const void* x, const v
     hipError_t e = launch_split_weights_3x3(conv_geom(d, ho, wo), wt, w3,
                                             d->in_dtype == OLLIE_BF16, s);
     if (e != hipSuccess) return hip_fail(e, "weight split launch");
-    st = conv_common(&q.d3, 0, x, w3, z, inner, ws_bytes - w3_bytes - z_bytes, flags, nullptr,
-                     stream);
+    if (!fused3) {
+        e = launch_gemm_nt(m, 9 * q.d3.k, d->c, x, w3, z, d->in_dtype == OLLIE_BF16, y_bf16,
+                           gemm_tile(flags), s);
+        if (e != hipSuccess) return hip_fail(e, "3x3 stage GEMM launch");
+        e = launch_eop_split3_chain(conv_geom(d, ho, wo), z, y_bf16, out,
+                                    d->out_dtype == OLLIE_BF16, epi, s);
+        if (e != hipSuccess) return hip_fail(e, "fused eOperator chain launch");
+        return OLLIE_OK;
+    }
+    st = conv_common(&q.d3, 0, x, w3, z, nullptr, 0, flags, nullptr, stream);
     if (st) return st;
     ConvGeom gb = conv_geom(d, ho, wo);
     gb.h = hz;

@@ -151,6 +151,12 @@ struct ConvGeom {
 hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, int y_bf16,
                              void* out, int out_bf16, const Epi& epi, hipStream_t stream);
 
+// The R x S -> 3x3 derived form's two eOperators (the 3x3 stage's OffsetAdd and the
+// block OffsetAdd) fused into one OffsetAdd over the split form's scope
+// Y [n*h*w][9*ceil(R/3)*ceil(S/3)*K] (g: the original stride-1 convolution).
+hipError_t launch_eop_split3_chain(const ConvGeom& g, const void* y, int y_bf16, void* out,
+                                   int out_bf16, const Epi& epi, hipStream_t stream);
+
 // Fused GEMM + eOperator (output-stationary), bf16 operands.  form: the derived
 // program evaluated -- the forward convolution, the transposed convolution, or a
 // stride-1 dilated convolution as dil_h*dil_w non-dilated convolutions over the

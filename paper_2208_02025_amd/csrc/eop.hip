@@ -180,6 +180,90 @@ __global__ __launch_bounds__(256) void eop_taps_kernel(const YT* __restrict__ Y,
     Out<OT>::put4(out + oi, epi_apply4(epi, acc, oi, k));
 }
 
+// The two consecutive eOperators of the R x S -> 3x3 derived form fused into one
+// (eOperator fusion, section 5.4).  That form computes Y = X * W3^T with the split
+// weights W3[r'][s'][(a*nbs + b)*K + k] = Wt[3a + r'][3b + s'][k], then
+//   Z[n][i][j][(a,b),k] = sum_{r',s'} Y[(n, i - ph - er + r', j - pw - es + s')][(r'*3+s')*nbr*nbs*K + (a,b)*K + k]
+//   out[n][ho][wo][k]   = sum_{a,b} Z[n][ho + er + 3a][wo + es + 3b][(a,b),k].
+// Substituting the first into the second (the shifts er, es cancel) gives one
+// OffsetAdd over Y:
+//   out[n][ho][wo][k] = sum_{a,b,r',s'} [0 <= hi < h][0 <= wi < w]
+//                       Y[(n*h + hi)*w + wi][((r'*3 + s')*nbr*nbs + a*nbs + b)*K + k]
+//   hi = ho - ph + 3a + r',  wi = wo - pw + 3b + s'.
+// Taps of the relaxed kernel (3a + r' >= R or 3b + s' >= S) have zero weights, so their
+// partials are zero and are not read (boundary tightening): the loop runs over the R x S
+// taps r = 3a + r', s = 3b + s'.  Y is read once and Z never exists.  Stride 1,
+// dilation 1 (the form's domain).
+template <typename YT, typename OT, int VEC>
+__global__ __launch_bounds__(256) void eop_split3_chain_kernel(const YT* __restrict__ Y,
+                                                               OT* __restrict__ out, ConvGeom g,
+                                                               int64_t total, Epi epi) {
+    const int64_t item = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (item >= total) return;
+    const int kv = (int)(g.k / VEC);
+    const int ho_n = (int)g.ho, wo_n = (int)g.wo;
+    const int it = (int)item;   // total < 2^31 (checked on the host)
+    const int k = (it % kv) * VEC;
+    int pix = it / kv;
+    const int wo = pix % wo_n;
+    pix /= wo_n;
+    const int ho = pix % ho_n;
+    const int n = pix / ho_n;
+    const int H = (int)g.h, W = (int)g.w, R = (int)g.r, S = (int)g.s, K = (int)g.k;
+    const int nbs = (S + 2) / 3, nb = ((R + 2) / 3) * nbs;
+    const int64_t nc = (int64_t)9 * nb * K;   // row length of Y
+
+    float acc[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
+    for (int r = 0; r < R; ++r) {
+        const int hi = ho - g.ph + r;
+        if (hi < 0 || hi >= H) continue;
+        const int a = r / 3, rr = r - 3 * a;
+        for (int s = 0; s < S; ++s) {
+            const int wi = wo - g.pw + s;
+            if (wi < 0 || wi >= W) continue;
+            const int b = s / 3, ss = s - 3 * b;
+            const int64_t row = ((int64_t)n * H + hi) * W + wi;
+            const YT* src = Y + row * nc + ((int64_t)(rr * 3 + ss) * nb + a * nbs + b) * K + k;
+            if (VEC == 4) {
+                f32x4 v = In<YT>::get4(src);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc[e] += In<YT>::get(src + e);
+            }
+        }
+    }
+    const int64_t oi = (((int64_t)n * ho_n + ho) * wo_n + wo) * K + k;
+    OT* dst = out + oi;
+    if (VEC == 4) {
+        f32x4 v = {acc[0], acc[1], acc[2], acc[3]};
+        Out<OT>::put4(dst, epi_apply4(epi, v, oi, k));
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            Out<OT>::put(dst + e, epi_apply(epi, acc[e], oi + e, k + e));
+    }
+}
+
+template <typename YT, typename OT>
+hipError_t go_chain(const ConvGeom& g, const void* y, void* out, const Epi& epi,
+                    hipStream_t st) {
+    const bool v4 = (g.k & 3) == 0;
+    const int64_t total = g.n * g.ho * g.wo * (v4 ? g.k / 4 : g.k);
+    if (total == 0) return hipSuccess;
+    const dim3 grid((unsigned)((total + 255) / 256));
+    if (v4)
+        hipLaunchKernelGGL((eop_split3_chain_kernel<YT, OT, 4>), grid, dim3(256), 0, st,
+                           (const YT*)y, (OT*)out, g, total, epi);
+    else
+        hipLaunchKernelGGL((eop_split3_chain_kernel<YT, OT, 1>), grid, dim3(256), 0, st,
+                           (const YT*)y, (OT*)out, g, total, epi);
+    return hipGetLastError();
+}
+
 int gcd_int(int a, int b) {
     while (b) {
         const int t = a % b;
@@ -250,6 +334,15 @@ hipError_t launch_eop_gather(const ConvGeom& g, int transposed, const void* y, i
                         : pick_vec<bf16_t, float>(g, transposed, y, out, epi, stream);
     return out_bf16 ? pick_vec<float, bf16_t>(g, transposed, y, out, epi, stream)
                     : pick_vec<float, float>(g, transposed, y, out, epi, stream);
+}
+
+hipError_t launch_eop_split3_chain(const ConvGeom& g, const void* y, int y_bf16, void* out,
+                                   int out_bf16, const Epi& epi, hipStream_t stream) {
+    if (y_bf16)
+        return out_bf16 ? go_chain<bf16_t, bf16_t>(g, y, out, epi, stream)
+                        : go_chain<bf16_t, float>(g, y, out, epi, stream);
+    return out_bf16 ? go_chain<float, bf16_t>(g, y, out, epi, stream)
+                    : go_chain<float, float>(g, y, out, epi, stream);
 }
 
 }  // namespace ollie

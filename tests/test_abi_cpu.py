@@ -280,11 +280,12 @@ def test_split3x3_flag_rejections_and_workspace(lib):
     assert call_conv(lib, "derived_conv2d", conv(c=12, r=5, s=5, pad=2),
                      flags=S)[0] == ol.EALIGN            # bf16 rows of 24 bytes
     assert call_conv(lib, "derived_conv2d", d5, out=MIS, flags=S)[0] == ol.EALIGN
-    # W3 [3][3][4*16][64] bf16 + Z [1][18][18][64] fp32 + the 3x3 stage's Y (two-stage)
+    # W3 [3][3][4*16][64] bf16, then Z [1][18][18][64] fp32 (fused 3x3 stage) or the 3x3
+    # stage's scope Y [14*14][9*64] (GEMM stage; its two eOperators run fused, no Z)
     w3, z, y = 9 * 64 * 64 * 2, 18 * 18 * 64 * 4, 14 * 14 * 9 * 64 * 4
-    assert ol.conv_workspace_bytes(d5, False, S) == w3 + z + y
+    assert ol.conv_workspace_bytes(d5, False, S) == w3 + y
     assert ol.conv_workspace_bytes(d5, False, S | ol.FUSE_EPILOGUE) == w3 + z
-    assert ol.conv_workspace_bytes(d5, False, S | ol.Y_BF16) == w3 + z + y // 2
+    assert ol.conv_workspace_bytes(d5, False, S | ol.Y_BF16) == w3 + y // 2
     assert ol.conv_workspace_bytes(d5, True, S) == 0
     # a 4x2 kernel: blocks 2x1, relaxed taps er = 2, es = 1: Z is (14+2*3-2) x (14+2*2-2)
     d42 = conv(c=64, r=4, s=2, pad=1)

@@ -255,15 +255,55 @@ def test_srcnn_workload_direct_and_split_sampled(integer):
                for q in (0, 1, wo - 2, wo - 1) for kk in (0, wl.k - 1)]
     idx = np.unique(np.concatenate([idx, np.array(corners)]))
     ref = oracle.conv2d(x, wt, wl.stride, wl.pad, 1, idx=idx)
-    for split in (False, True):
-        out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), wl.stride, wl.pad, fuse=True,
+    # direct (fused 25 taps); split with the fused 3x3 stage; split with the 3x3 stage's
+    # GEMM and its two eOperators fused into one (no Z)
+    for split, fuse in ((False, True), (True, True), (True, False)):
+        out = ol.derived_conv2d(x.to(DEV), wt.to(DEV), wl.stride, wl.pad, fuse=fuse,
                                 split3x3=split)
         torch.cuda.synchronize()
         got = to_np(out).reshape(-1)[idx]
+        del out
         if integer:
-            assert np.array_equal(got, ref), split
+            assert np.array_equal(got, ref), (split, fuse)
         else:
-            assert err(got, ref) <= TOL_BF16, split
+            assert err(got, ref) <= TOL_BF16, (split, fuse)
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("ci", [0, 1, 3, 5])
+@pytest.mark.parametrize("out_bf16", [False, True])
+def test_split3x3_fused_eoperator_chain(ci, out_bf16):
+    """The split form's two consecutive eOperators fused into one kernel over the 3x3
+    stage's scope (OLLIE_CONV_SPLIT_3X3 without OLLIE_FUSE_EPILOGUE): its workspace has
+    no Z, and on integer inputs with a bias + ReLU tail it is exactly the definition and
+    equal to the split form through Z (fused 3x3 stage, where covered); with a bf16
+    scope, within the bf16 tolerance."""
+    n, c, h, w, k, r, s, pad, dt = SPLIT3_GPU_CASES[ci]
+    say("split3x3 fused chain", SPLIT3_GPU_CASES[ci], "bf16 out" if out_bf16 else "fp32 out")
+    od = torch.bfloat16 if out_bf16 else torch.float32
+    x = synth.random_tensor((n, h, w, c), 11400 + ci, dt, integer=True)
+    wt = synth.random_tensor((r, s, k, c), 11500 + ci, dt, integer=True)
+    bias = synth.random_tensor((k,), 11600 + ci, integer=True)
+    desc = ol.conv_desc(tuple(x.shape), tuple(wt.shape), 1, pad, 1, 0, x.dtype, od)
+    nb = ((r + 2) // 3) * ((s + 2) // 3)
+    el = 2 if dt == "bf16" else 4
+    w3_bytes = (9 * nb * k * c * el + 255) // 256 * 256
+    assert ol.conv_workspace_bytes(desc, False, ol.CONV_SPLIT_3X3) == \
+        w3_bytes + n * h * w * 9 * nb * k * 4
+    ref = oracle.conv_epilogue(oracle.conv2d(x, wt, 1, pad, 1), bias, None, True)
+    xg, wg, bg = x.to(DEV), wt.to(DEV), bias.to(DEV)
+    out = ol.derived_conv2d(xg, wg, 1, pad, out_dtype=od, split3x3=True, bias=bg, relu=True)
+    via_z = ol.derived_conv2d(xg, wg, 1, pad, out_dtype=od, split3x3=True, fuse=True,
+                              bias=bg, relu=True)
+    torch.cuda.synchronize()
+    if out_bf16:
+        assert torch.equal(out.cpu(), torch.from_numpy(ref).to(torch.bfloat16))
+    else:
+        assert np.array_equal(to_np(out), ref)
+    assert torch.equal(out, via_z)
+    out = ol.derived_conv2d(xg, wg, 1, pad, y_bf16=True, split3x3=True)
+    torch.cuda.synchronize()
+    assert err(to_np(out), oracle.conv2d(x, wt, 1, pad, 1)) <= TOL_BF16
 
 
 def test_split3x3_float_tail_bf16_out_and_bf16_scope():

@@ -245,6 +245,46 @@ def test_split3x3_derived_form_exact_on_integers(ci):
     assert np.array_equal(got, ref)
 
 
+@pytest.mark.parametrize("ci", range(len(SPLIT3_CASES)))
+def test_split3x3_fused_eoperator_chain_exact_on_integers(ci):
+    """The 3x3 derived form with its two consecutive eOperators fused into one over the
+    3x3 stage's scope (no intermediate Z) equals the convolution's definition and the
+    unfused chain (3x3 OffsetAdd into Z, then the block OffsetAdd) exactly on integer
+    inputs; on real-valued inputs all three agree to float64 rounding."""
+    n, c, h, w, k, r, s, pad = SPLIT3_CASES[ci]
+    x = synth.random_tensor((n, h, w, c), 1200 + ci, integer=True).numpy()
+    wt = synth.random_tensor((r, s, k, c), 1300 + ci, integer=True).numpy()
+    got = dfm.derived_conv2d_split3x3_chain(x, wt, pad)
+    ref = oracle.conv2d(x, wt, 1, pad, 1)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
+    assert np.array_equal(got, dfm.derived_conv2d_split3x3(x, wt, pad))
+    xf = synth.random_tensor((n, h, w, c), 1250 + ci).numpy()
+    wf = synth.random_tensor((r, s, k, c), 1350 + ci).numpy()
+    got = dfm.derived_conv2d_split3x3_chain(xf, wf, pad)
+    ref = oracle.conv2d(xf, wf, 1, pad, 1)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12 * max(1.0, np.abs(ref).max()))
+
+
+def test_split3x3_chain_reads_each_tap_of_the_kernel_once():
+    """A lone 1 in the input and a kernel whose entries are distinct powers of two: the
+    fused chain's output at every position is the sum of the kernel entries whose tap
+    lands on the 1, so each real tap (r, s) is read exactly once and no relaxed tap
+    contributes (a dropped or doubled tap changes the binary digits)."""
+    r_n, s_n, h, w = 5, 4, 9, 8
+    x = np.zeros((1, h, w, 1))
+    x[0, 4, 3, 0] = 1.0
+    wt = (2.0 ** np.arange(r_n * s_n)).reshape(r_n, s_n, 1, 1)
+    got = dfm.derived_conv2d_split3x3_chain(x, wt, (2, 1))
+    ho_n, wo_n = h + 4 - r_n + 1, w + 2 - s_n + 1
+    assert got.shape == (1, ho_n, wo_n, 1)
+    for ho in range(ho_n):
+        for wo in range(wo_n):
+            r, s = 4 - ho + 2, 3 - wo + 1          # the tap whose input pixel is (4, 3)
+            want = wt[r, s, 0, 0] if 0 <= r < r_n and 0 <= s < s_n else 0.0
+            assert got[0, ho, wo, 0] == want, (ho, wo)
+
+
 def test_split3x3_weights_cover_every_tap_once():
     """Each tap of the kernel lands in exactly one (block, r', s') slot of W3 and the
     relaxed slots are zero: the block sums of W3 reproduce the kernel's total per
