@@ -410,6 +410,69 @@ def split_iter(prog: Program, name: str, it: str, block: int, a: str, b: str) ->
     return None
 
 
+def residue_split(prog: Program, name: str, it: str, D: int, ip: str = "ip",
+                  rho: str = "rho") -> Optional[Program]:
+    """Variable substitution it = D*ip + rho (ip outer, rho inner) on a traversal
+    iterator of range [0, n*D), with the data layout transformation that goes with it
+    (section 5.2: T'[x'] = T[Phi(x')]).  Every operand index that uses `it` must read
+    an input's dimension as it + D*e + c with e free of `it` and c a multiple of D;
+    such an input is read through its residue view
+        TR[.., rho, t', ..] = T[.., D*t' + rho, ..]
+    (an identity eOperator: a strided view), where the index becomes ip + e + c/D.  The
+    contraction moves to a new scope traversing (.., rho, ip, ..) with rho placed before
+    the row, and the original scope, its traversal split in place as (.., ip, rho, ..)
+    (the same memory layout), reads it back."""
+    s = prog.scope(name)
+    tn = [i.name for i in s.trav]
+    if it not in tn or ip in s.ranges() or rho in s.ranges() or D < 2 or prog.parents(name):
+        return None
+    pos = tn.index(it)
+    itr = s.trav[pos]
+    if itr.lo != 0 or itr.hi % D:
+        return None
+    shapes = dict(prog.inputs)
+    n = itr.hi // D
+    views: Dict[str, Scope] = {}
+    refs = []
+    for r in s.refs:
+        dims = [d for d, a in enumerate(r.idx) if a.coef(it)]
+        if not dims:
+            refs.append(r)
+            continue
+        if len(dims) != 1 or r.tensor not in shapes:
+            return None
+        d = dims[0]
+        a = r.idx[d]
+        if isinstance(a, Quot) or a.coef(it) != 1 or a.const % D:
+            return None
+        e = a - Aff.var(it) - a.const
+        if any(c % D for _, c in e.terms):
+            return None
+        shp = shapes[r.tensor]
+        if shp[d] % D:
+            return None
+        vname = r.tensor + "R"
+        vit = ["v%d" % m for m in range(len(shp))]
+        vtrav = tuple(Iter(vit[m], 0, shp[m]) for m in range(d)) + \
+            (Iter("vr", 0, D), Iter("vq", 0, shp[d] // D)) + \
+            tuple(Iter(vit[m], 0, shp[m]) for m in range(d + 1, len(shp)))
+        vidx = tuple(Aff.var(vit[m]) for m in range(d)) + (Aff.of({"vq": D, "vr": 1}),) + \
+            tuple(Aff.var(vit[m]) for m in range(d + 1, len(shp)))
+        views[vname] = Scope(vtrav, (), (Ref(r.tensor, vidx),))
+        e_div = Aff.of({k: c // D for k, c in e.terms}, a.const // D)
+        idx = r.idx[:d] + (Aff.var(rho), Aff.var(ip) + e_div) + r.idx[d + 1:]
+        refs.append(Ref(vname, idx))
+    if not views or any(v in dict(prog.scopes) for v in views):
+        return None
+    gname = prog.fresh("G")
+    gtrav = s.trav[:pos] + (Iter(rho, 0, D), Iter(ip, 0, n)) + s.trav[pos + 1:]
+    g = Scope(gtrav, s.sums, tuple(refs), s.guards)
+    otrav = s.trav[:pos] + (Iter(ip, 0, n), Iter(rho, 0, D)) + s.trav[pos + 1:]
+    oidx = tuple(Aff.var(i.name) for i in gtrav)
+    outer = Scope(otrav, (), (Ref(gname, oidx),))
+    return prog.with_scopes(**{name: outer, gname: g}, **views)
+
+
 def _box(prog: Program, tensor: str, dim: int) -> Tuple[int, int]:
     shapes = dict(prog.inputs)
     if tensor in shapes:
@@ -666,28 +729,37 @@ def match_conv(prog: Program, name: str) -> Optional[Match]:
 
 
 def match_g2bmm(prog: Program, name: str) -> Optional[Match]:
-    """G2BMM: all = (b, i), wo = (j), iw = (d); input Q[b, i, d], weight
-    K[b, i + D*(j - w), d]: a band of width 2w+1 with dilation D."""
+    """G2BMM (Table 2): iterators in all three tensors (the batch iterators and the row
+    i, last), the band offset j in weight+output, the contraction d in input+weight;
+    input Q[batch.., i, d], weight K[batch.., i + D*(j - w), d]: a band of width 2w+1
+    with dilation D (D = 1 is the non-dilated band)."""
     g = mapping_table(prog, name)
-    if g is None or len(g["all"]) != 2 or len(g["wo"]) != 1 or len(g["iw"]) != 1 or g["io"]:
+    if g is None or len(g["all"]) < 2 or len(g["wo"]) != 1 or len(g["iw"]) != 1 or g["io"]:
         return None
     s = prog.scope(name)
     q, k = s.refs
-    b_, i_ = g["all"]
+    batch, i_ = g["all"][:-1], g["all"][-1]
     j_, d_ = g["wo"][0], g["iw"][0]
-    if [x.iters() for x in q.idx] != [(b_,), (i_,), (d_,)] or k.idx[0] != Aff.var(b_):
+    nb = len(batch)
+    if [x.iters() for x in q.idx] != [(x,) for x in batch] + [(i_,), (d_,)]:
         return None
-    t = k.idx[1]
+    if any(q.idx[m] != Aff.var(batch[m]) or k.idx[m] != Aff.var(batch[m]) for m in range(nb)):
+        return None
+    if len(k.idx) != nb + 2 or q.idx[nb] != Aff.var(i_) or q.idx[nb + 1] != Aff.var(d_):
+        return None
+    t = k.idx[nb]
+    if isinstance(t, Quot):
+        return None
     D = t.coef(j_)
-    if t.coef(i_) != 1 or D <= 0 or set(t.iters()) != {i_, j_} or k.idx[2] != Aff.var(d_):
+    if t.coef(i_) != 1 or D <= 0 or set(t.iters()) != {i_, j_} or k.idx[nb + 1] != Aff.var(d_):
         return None
     rng = s.ranges()
     wj = rng[j_]
     if t.const + D * wj[0] > 0 or (-t.const) % D:
         return None
-    return Match("G2BMM", name, {"all": [b_, i_], "wo": [j_], "iw": [d_]},
+    return Match("G2BMM", name, {"all": list(g["all"]), "wo": [j_], "iw": [d_]},
                  {"dilation": D, "w": (-t.const) // D - wj[0], "band": wj[1] - wj[0],
-                  "L": rng[i_][1] - rng[i_][0]})
+                  "L": rng[i_][1] - rng[i_][0], "row": i_, "batch": list(batch)})
 
 
 MATCHERS = {"Matmul": match_matmul, "Conv": match_conv, "G2BMM": match_g2bmm}
@@ -727,6 +799,16 @@ def _moves_all(prog: Program):
             p = _try(eliminate_guard, prog, name, x)
             if p is not None:
                 yield ("eliminate", name, x), p
+        # data layout changes: variable substitution by a transposition of two
+        # neighbouring traversal iterators of an instantiated scope (the program's
+        # result keeps its layout)
+        if name != prog.out:
+            tn_ = [i.name for i in s.trav]
+            for k in range(len(tn_) - 1):
+                order = tn_[:k] + [tn_[k + 1], tn_[k]] + tn_[k + 2:]
+                p = _try(permute, prog, name, order)
+                if p is not None:
+                    yield ("swap", name, tn_[k], tn_[k + 1]), p
         # substitution candidates: a multi-iterator index expression over this
         # scope's traversal iterators becomes a new iterator
         tn = {i.name for i in s.trav}
@@ -752,18 +834,148 @@ class Derived:
     steps: List[tuple]
     matches: List[Match]
     eops: List[str]
+    guided: int = 0               # how many of the steps (the last ones) were guided
+
+
+def _plain(a: Aff) -> Optional[str]:
+    """The iterator of an index that is that iterator alone, else None."""
+    if isinstance(a, Quot) or len(a.terms) != 1 or a.terms[0][1] != 1 or a.const:
+        return None
+    return a.terms[0][0]
+
+
+def derived_match(prog: Program, target: str) -> Optional[Match]:
+    """The program is a derived program for `target` when one scope is that operator in
+    the exact form a kernel takes (Matmul: operand and output layouts of Eq. (3) and
+    (4), read by an eOperator; G2BMM: a non-dilated band) and every other scope is an
+    eOperator or a view.  Returns the operator's match."""
+    for name, _ in prog.scopes:
+        m = MATCHERS[target](prog, name)
+        if m is None:
+            continue
+        if target == "Matmul" and (m.detail.get("reordered") or name == prog.out or
+                                   len(prog.scopes) < 2):
+            continue
+        if target == "G2BMM" and m.detail["dilation"] != 1:
+            continue
+        return m
+    return None
+
+
+def select_rules(prog: Program, target: str) -> List[Tuple[tuple, Program]]:
+    """The guided stage's choice of rules (section 5.2, Alg. 2 SelectRules): the
+    mismatches between the iterator mapping table of each two-operand scope with a
+    summation and the target's iterator groups (Table 2) decide what to apply, the
+    first kind that applies per scope, in this order:
+      * contraction-group mismatch: summation iterators other than the plain indices
+        that both operands share (they also shift an input index, or a guard uses
+        them) -- summation splitting keeps only the shared ones inside;
+      * iterator-group mismatch: a traversal iterator coupled with another iterator in
+        one index (the group needs single iterators) -- variable substitution merges
+        the index into one new iterator; then boundary tightening shrinks the new
+        iterator to the tensor's box;
+      * a band whose weight index has dilation D > 1 (G2BMM): the row iterator is split
+        by residue and the operands are read through residue views (a data layout
+        transformation), which makes the band non-dilated;
+      * data-layout mismatch (Matmul): the scope's traversal order differs from the
+        target's (m, n) output layout -- a permutation of its traversal."""
+    moves: List[Tuple[tuple, Program]] = []
+    for name, s in prog.scopes:
+        if len(s.refs) != 2 or not s.sums:
+            continue
+        a, b = s.refs
+        shared = [i.name for i in s.sums
+                  if any(_plain(x) == i.name for x in a.idx) and
+                  any(_plain(x) == i.name for x in b.idx) and
+                  not any(g.aff.coef(i.name) for g in s.guards)]
+        if shared and len(shared) < len(s.sums):
+            q = _try(split_summation, prog, name, shared)
+            if q is not None:
+                moves.append((("split", name, tuple(shared)), q))
+                continue
+        if s.guards:
+            continue                              # a guarded scope stays an eOperator
+        tn = [i.name for i in s.trav]
+        found = False
+        for r, other in ((a, b), (b, a)):
+            used_other = {k for y in other.idx for k in y.iters()}
+            for x in r.idx:
+                if isinstance(x, Quot) or len(x.terms) < 2 or not set(x.iters()) <= set(tn):
+                    continue
+                olds = [k for k in x.iters() if k not in used_other]
+                if len(olds) != 1:
+                    continue
+                taken = set(s.ranges())
+                fresh = next("t%d" % k for k in itertools.count() if "t%d" % k not in taken)
+                q = _try(substitute, prog, name, olds[0], x, fresh)
+                if q is not None:
+                    moves.append((("subst", name, olds[0], str(x)), q))
+                    found = True
+                    break
+            if found:
+                break
+        if found:
+            continue
+        q = _try(tighten, prog, name)
+        if q is not None:
+            moves.append((("tighten", name), q))
+            continue
+        if target == "G2BMM":
+            m = match_g2bmm(prog, name)
+            if m is not None and m.detail["dilation"] > 1:
+                q = _try(residue_split, prog, name, m.detail["row"], m.detail["dilation"])
+                if q is not None:
+                    moves.append((("residue", name, m.detail["row"], m.detail["dilation"]), q))
+                    continue
+        if target == "Matmul":
+            m = match_matmul(prog, name)
+            if m is not None and m.detail.get("reordered"):
+                q = _try(permute, prog, name, m.detail["order"])
+                if q is not None:
+                    moves.append((("permute", name, tuple(m.detail["order"])), q))
+    return moves
+
+
+def guided_derive(prog: Program, target: str, steps: List[tuple], found: List[Derived],
+                  found_fp: set, budget: int = 8, stats: Optional[Dict[str, int]] = None,
+                  _seen: Optional[set] = None, _depth: int = 0):
+    """Guided derivation of one program toward `target` (Alg. 2 GuidedDerive): a
+    program that is derived (one target operator, the rest eOperators) is recorded;
+    otherwise each rule select_rules picks is applied and the result derived further,
+    up to `budget` guided steps."""
+    seen = set() if _seen is None else _seen
+    m = derived_match(prog, target)
+    if m is not None:
+        fp = fingerprint(prog)
+        if fp not in found_fp:
+            found_fp.add(fp)
+            found.append(Derived(prog, steps, [m], [n for n, _ in prog.scopes if n != m.scope],
+                                 _depth))
+        return
+    if budget <= 0:
+        return
+    for mv, q in select_rules(prog, target):
+        fq = fingerprint(q)
+        if fq in seen:
+            continue
+        seen.add(fq)
+        if stats is not None:
+            stats["guided"] = stats.get("guided", 0) + 1
+        guided_derive(q, target, steps + [mv], found, found_fp, budget - 1, stats, seen,
+                      _depth + 1)
 
 
 def derive(prog: Program, targets: Sequence[str] = ("Matmul",), max_depth: int = 4,
            max_states: int = 20000, prune: bool = True,
-           stats: Optional[Dict[str, int]] = None) -> List[Derived]:
-    """Breadth-first search over rule applications up to `max_depth`, skipping
-    programs whose fingerprint was seen (prune=False explores them again; `stats`
-    receives the counts of states explored and pruned); every state is checked against the target
-    operators through the mapping table.  A state is a derived program when one
-    scope that carries a summation over the operator's contraction is matched and
-    every other scope is an eOperator (no scope of its own left to match).  Results
-    are returned in the order found (shallowest first)."""
+           stats: Optional[Dict[str, int]] = None, guided: bool = True,
+           guided_budget: int = 8) -> List[Derived]:
+    """Hybrid derivation (section 5.2, Alg. 2): breadth-first explorative derivation
+    (every rule on every state) up to `max_depth`, skipping programs whose fingerprint
+    was seen (prune=False explores them again); from every explorative state, guided
+    derivation toward each target (guided=False: the state itself is only checked for a
+    derived program, i.e. explorative derivation alone).  `stats` receives the counts of
+    explorative states, pruned states and guided rule applications.  Results are
+    returned in the order found (shallowest explorative depth first)."""
     seen = set()
     queue = [(prog, [])]
     found: List[Derived] = []
@@ -784,20 +996,14 @@ def derive(prog: Program, targets: Sequence[str] = ("Matmul",), max_depth: int =
             if states > max_states:
                 return found
             for t in targets:
-                for name, s in p.scopes:
-                    m = MATCHERS[t](p, name)
-                    if m is None or len(p.scopes) < 2 or name == p.out:
-                        continue
-                    q, st = p, steps
-                    if m.detail.get("reordered"):
-                        # guided step: the layout the operator needs (Eq. 3 / Eq. 4)
-                        q = permute(p, name, m.detail["order"])
-                        st = steps + [("permute", name, tuple(m.detail["order"]))]
-                        m = MATCHERS[t](q, name)
-                    fq = fingerprint(q)
-                    if fq not in found_fp:
-                        found_fp.add(fq)
-                        found.append(Derived(q, st, [m], [n for n, _ in q.scopes if n != name]))
+                if guided:
+                    guided_derive(p, t, steps, found, found_fp, guided_budget, stats)
+                else:
+                    m = derived_match(p, t)
+                    if m is not None and fp not in found_fp:
+                        found_fp.add(fp)
+                        found.append(Derived(p, steps, [m],
+                                             [n for n, _ in p.scopes if n != m.scope]))
             if len(steps) < max_depth:
                 for mv, q in _moves(p):
                     nxt.append((q, steps + [mv]))
@@ -878,18 +1084,42 @@ def _axis(idx: Aff, o: str, r: str, transposed: bool) -> Tuple[int, int, int]:
     return den, num.const, -num.coef(r)
 
 
+def _gather_form(prog: Program, eop: str, pixel: Sequence[str]) -> Tuple[Program, List[tuple]]:
+    """The eOperator in the form its kernel evaluates (the eOperator generation of
+    section 4.3.2): each summation iterator that reads a pixel coordinate of the scope
+    (`pixel`) and that an equality guard determines is eliminated, so the kernel sums
+    over the taps and gathers the partials that land on an output instead of searching
+    the input space for them (the selective add)."""
+    steps = []
+    for x in pixel:
+        if x not in {i.name for i in prog.scope(eop).sums}:
+            continue
+        q = _try(eliminate_guard, prog, eop, x)
+        if q is None:
+            continue
+        steps.append(("eliminate", eop, x))
+        prog = q
+    return prog, steps
+
+
 def derive_conv(prog: Program, transposed: bool = False,
-                max_depth: int = 4) -> Tuple[ConvPlan, Derived]:
-    """Derive a convolution-family expression to Matmul + eOperator and read the
-    eOperator's tap map off the derived expression."""
+                max_depth: int = 0) -> Tuple[ConvPlan, Derived]:
+    """Derive a convolution-family expression to Matmul + eOperator by hybrid
+    derivation (explorative up to `max_depth`, guided from every state), bring the
+    eOperator to its gather form, and read its tap map off the derived expression."""
     res = derive(prog, ("Matmul",), max_depth=max_depth)
     for dv in res:
         m = dv.matches[0]
-        p = dv.prog
-        outer = [s for n, s in p.scopes if n != m.scope]
-        if len(outer) != 1:
+        outer_names = [n for n, _ in dv.prog.scopes if n != m.scope]
+        if len(outer_names) != 1:
             continue
-        eop = outer[0]
+        ref = [r for r in dv.prog.scope(outer_names[0]).refs if r.tensor == m.scope]
+        if len(ref) != 1:
+            continue
+        tpos = {i.name: k for k, i in enumerate(dv.prog.scope(m.scope).trav)}
+        pixel = [x for k in m.groups["m"] for x in ref[0].idx[tpos[k]].iters()]
+        p, more = _gather_form(dv.prog, outer_names[0], pixel)
+        eop = p.scope(outer_names[0])
         # the eOperator reads Y once per tap; Y is the only operand
         if len(eop.refs) != 1 or eop.refs[0].tensor != m.scope:
             continue
@@ -906,7 +1136,7 @@ def derive_conv(prog: Program, transposed: bool = False,
             continue
         plan = ConvPlan(m.detail["M"], m.detail["N"], m.detail["K"], m.groups["m"],
                         m.groups["n"], m.groups["k"], tr, (sh, sw), (ph, pw), (dh, dw))
-        return plan, dv
+        return plan, Derived(p, dv.steps + more, dv.matches, dv.eops, dv.guided)
     raise ValueError("no Matmul + eOperator program within depth %d" % max_depth)
 
 
@@ -920,25 +1150,38 @@ class BandPlan:
 
 
 def derive_band(b: int, l: int, d: int, w: int, dil: int) -> Tuple[BandPlan, Match, Match]:
-    """The dilated G2BMM matches the G2BMM pattern with dilation D; substituting
-    i = D*i' + rho turns every residue into a band of dilation 1 over the strided
-    subsequence (the dilated-to-non-dilated rewrite of section 6.4)."""
-    p = g2bmm_expr(b, l, d, w, dil)
-    m0 = match_g2bmm(p, "E")
+    """The dilated G2BMM matches the G2BMM pattern with dilation D.  Hybrid derivation
+    toward the non-dilated G2BMM splits the row iterator by residue, i = D*i' + rho,
+    and reads Q and K through residue views, turning every residue into a band of
+    dilation 1 over the strided subsequence (the dilated-to-non-dilated rewrite of
+    section 6.4).  The residue split needs a whole number of rows per residue, so the
+    derivation runs on the l rounded up to a multiple of D (rows past l read the zero
+    padding and are never stored); the plan's residue lengths are those of l itself."""
+    m0 = match_g2bmm(g2bmm_expr(b, l, d, w, dil), "E")
     if m0 is None:
         raise ValueError("not a G2BMM")
-    res = []
-    m1 = None
-    for rho in range(dil):
-        n = (l - rho + dil - 1) // dil
-        if n <= 0:
-            continue
-        sub = _residue_band(b, l, d, w, dil, rho, n)
-        m1 = match_g2bmm(sub, "E")
-        if m1 is None or m1.detail["dilation"] != 1:
-            raise ValueError("residue %d is not a non-dilated band" % rho)
-        res.append((rho, dil, n))
-    return BandPlan(dil, w, res), m0, m1
+    lr = -(-l // dil) * dil
+    res = derive(g2bmm_expr(b, lr, d, w, dil), ("G2BMM",), max_depth=0)
+    if not res:
+        raise ValueError("no non-dilated band derived")
+    m1 = res[0].matches[0]
+    if m1.detail["dilation"] != 1 or m1.detail["w"] != w:
+        raise ValueError("the derived band is not the non-dilated band of half-width w")
+    D = 1
+    for st in res[0].steps:
+        if st[0] == "residue":
+            D = st[3]
+    residues = [(rho, D, (l - rho + D - 1) // D) for rho in range(D) if l - rho > 0]
+    return BandPlan(D, w, residues), m0, m1
+
+
+def derive_band_program(b: int, l: int, d: int, w: int, dil: int) -> Derived:
+    """The hybrid derivation's program for the band (l a multiple of dil): the
+    non-dilated G2BMM over residue views, read back by the output in its own layout."""
+    res = derive(g2bmm_expr(b, l, d, w, dil), ("G2BMM",), max_depth=0)
+    if not res:
+        raise ValueError("no non-dilated band derived")
+    return res[0]
 
 
 def _residue_band(b, l, d, w, dil, rho, n) -> Program:
@@ -1032,3 +1275,25 @@ def conv_desc_fields(plan: ConvPlan, n: int, c: int, h: int, w: int, k: int, r: 
             "stride_h": plan.stride[0], "stride_w": plan.stride[1],
             "pad_h": plan.pad[0], "pad_w": plan.pad[1],
             "dil_h": plan.dil[0], "dil_w": plan.dil[1]}
+
+
+def conv_entry(plan: ConvPlan) -> str:
+    """The C ABI entry point that runs a derived convolution plan."""
+    if plan.transposed:
+        return "derived_conv_transpose2d"
+    return "derived_conv2d" if plan.dil == (1, 1) else "derived_dilated_conv2d"
+
+
+def split3_workspace_bytes(plan: Split3Plan, n: int, c: int, h: int, w: int, k: int,
+                           in_bytes: int, fused_stage: bool, y_bytes: int = 4) -> int:
+    """Workspace of the split form as the plan lays it out: the split weights
+    W3 [3][3][nbr*nbs*K][c], then (256-byte aligned) either the 3x3 stage's output Z
+    (fp32, extent h + 2*pad3 - 2) when that stage is the fused kernel, or its scope
+    Y [n*h*w][9*nbr*nbs*K] when its two eOperators run fused over Y."""
+    k3 = plan.nbr * plan.nbs * k
+    w3 = (9 * k3 * c * in_bytes + 255) // 256 * 256
+    if fused_stage:
+        hz, wz = h + 2 * plan.pad3[0] - 2, w + 2 * plan.pad3[1] - 2
+        return w3 + n * hz * wz * k3 * 4
+    return w3 + n * h * w * 9 * k3 * y_bytes
+

@@ -237,3 +237,87 @@ def test_quotient_index_arithmetic_is_exact_or_declines():
     ref = value(prog, t)
     for mv, q2 in D._moves(dv.prog):
         assert np.array_equal(value(q2, t), ref), mv
+
+
+# ---------------------------------------------------------------- guided derivation
+
+def test_guided_derivation_shortens_the_search():
+    """Hybrid derivation (section 5.2) against explorative derivation alone, as in
+    section 6.5: guided from the operator's own expression (explorative depth 0) the
+    targets are reached in a few guided steps, where explorative search alone needs
+    depth 6 (3x3 convolution), depth 5 (transposed convolution) or never reaches the
+    non-dilated band (its rules have no residue split), over thousands of states."""
+    conv = D.conv2d_expr(1, 2, 5, 5, 2, 3, 3, (1, 1), (1, 1))
+    convt = D.conv_transpose2d_expr(1, 2, 3, 3, 2, 4, 4, (2, 2), (1, 1))
+    band = D.g2bmm_expr(1, 8, 2, 2, 2)
+    for prog, target, guided_steps in ((conv, "Matmul", 5), (convt, "Matmul", 2),
+                                       (band, "G2BMM", 1)):
+        st = {}
+        res = D.derive(prog, (target,), max_depth=0, stats=st)
+        assert res and st["states"] == 1, target
+        assert res[0].guided == len(res[0].steps) == guided_steps
+        assert st["guided"] <= 2 * guided_steps
+    off = {}
+    assert not D.derive(conv, ("Matmul",), max_depth=5, guided=False, stats=off,
+                        max_states=10 ** 6)
+    assert off["states"] > 5000
+    off = {}
+    res = D.derive(conv, ("Matmul",), max_depth=6, guided=False, stats=off, max_states=10 ** 6)
+    assert res and len(res[0].steps) == 6 and off["states"] > 20000
+    off = {}
+    assert not D.derive(convt, ("Matmul",), max_depth=4, guided=False, stats=off)
+    res = D.derive(convt, ("Matmul",), max_depth=5, guided=False, stats=off)
+    assert res and len(res[0].steps) == 5 and off["states"] > 1000
+    assert not D.derive(band, ("G2BMM",), max_depth=3, guided=False)
+
+
+@pytest.mark.parametrize("pi", range(len(PROGS)))
+def test_every_guided_step_keeps_the_value(pi):
+    """Every program on every guided path from the operator's expression evaluates to
+    the original on a random integer instance (the band's derived program lays its
+    output out as (b, i', rho, j), the same memory as (b, i, j))."""
+    prog = PROGS[pi]
+    target = "G2BMM" if prog.inputs[0][0] == "Q" else "Matmul"
+    if target == "G2BMM":      # the residue split needs whole residues: 8 rows, dilation 2
+        prog = D.g2bmm_expr(1, 8, 2, 2, 2)
+    t = rand_inputs(prog, 700 + pi)
+    ref = value(prog, t)
+    frontier, seen = [prog], 0
+    for _ in range(6):
+        nxt = []
+        for p in frontier:
+            for mv, q in D.select_rules(p, target):
+                got = value(q, t)
+                assert np.array_equal(got.reshape(ref.shape), ref), mv
+                nxt.append(q)
+                seen += 1
+        frontier = nxt
+    assert seen >= 1
+    res = D.derive(prog, (target,), max_depth=0)
+    assert res and np.array_equal(value(res[0].prog, t).reshape(ref.shape), ref)
+
+
+def test_select_rules_follow_the_mapping_table_mismatches():
+    """On the convolution: first the contraction-group mismatch (r and s shift the input
+    index) -> split off c; then the coupled index ho + r - 1 -> substitute; then
+    tightening; then the layout -> permute to (m, n).  On the dilated band: the
+    dilation -> residue split into views QR, KR and a non-dilated G2BMM."""
+    p = D.conv2d_expr(1, 2, 5, 5, 2, 3, 3, (1, 1), (1, 1))
+    kinds = []
+    while True:
+        mv = D.select_rules(p, "Matmul")
+        if not mv or D.derived_match(p, "Matmul"):
+            break
+        assert len(mv) == 1
+        kinds.append(mv[0][0][0])
+        p = mv[0][1]
+    assert kinds == ["split", "subst", "subst", "tighten", "permute"]
+    m = D.derived_match(p, "Matmul")
+    assert m.groups == {"m": ["n", "t0", "t1"], "n": ["r", "s", "f"], "k": ["c"]}
+    b = D.g2bmm_expr(2, 8, 3, 2, 2)
+    (mv, q), = D.select_rules(b, "G2BMM")
+    assert mv[0] == "residue"
+    m = D.derived_match(q, "G2BMM")
+    assert m.detail["dilation"] == 1 and m.detail["w"] == 2 and m.detail["L"] == 4
+    assert {"QR", "KR"} <= {n for n, _ in q.scopes}
+    assert m.groups["all"] == ["b", "rho", "ip"]
