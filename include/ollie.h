@@ -71,7 +71,7 @@ typedef enum {
  *     (conv entry points; ignored when the call takes the two-stage path).
  *   OLLIE_GEMM_TILE(n), n in 0..4: tile shape of the GEMM stage kernel (conv entry
  *     points on the two-stage path; ignored on the fused path).
- *   OLLIE_BAND_SHAPE(n), n in 0..2: wave shape of the fused band kernel (banded_bmm
+ *   OLLIE_BAND_SHAPE(n), n in 0..3: wave shape of the fused band kernel (banded_bmm
  *     without OLLIE_BAND_STAGED).
  * An n outside its range gives OLLIE_EINVAL. */
 #define OLLIE_FUSED_TILE(n)     ((uint32_t)(((n) + 1) & 0xff) << 16)

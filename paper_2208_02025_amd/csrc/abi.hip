@@ -41,7 +41,7 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 // Tile-configuration override bits of the flags (0 = automatic, else config + 1).
 constexpr uint32_t kFusedTileBits = 0xffu << 16, kGemmTileBits = 0xfu << 24;
 constexpr uint32_t kBandShapeBits = 0xffu << 16;
-constexpr int kFusedTiles = 15, kGemmTiles = 5, kBandShapes = 3;
+constexpr int kFusedTiles = 15, kGemmTiles = 5, kBandShapes = 4;
 int fused_tile(uint32_t flags) { return (int)((flags & kFusedTileBits) >> 16) - 1; }
 int gemm_tile(uint32_t flags) { return (int)((flags & kGemmTileBits) >> 24) - 1; }
 int band_shape(uint32_t flags) { return (int)((flags & kBandShapeBits) >> 16) - 1; }

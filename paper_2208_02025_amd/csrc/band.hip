@@ -668,6 +668,274 @@ __global__ __launch_bounds__(64 * NW, HQ <= 2 ? 4 : 2) void band_fused_kernel(Ba
     }
 }
 
+// Half-block form of the fused kernel: the same tiles, ring and softmax bookkeeping as
+// band_fused_kernel with four waves of 32 queries, but every 64-key block is evaluated
+// as two 32-key halves, each scores -> softmax -> P*V on its own.  That halves the
+// score and key-fragment registers live at once (in zero mode five workgroups per CU
+// fit: 96 VGPRs, 5 x 32 KB of LDS; the range masks of mask mode need three to stay out
+// of scratch memory), and a half
+// that lies outside the band of every query of the wave
+// is skipped (the band of 32 queries spans 32 + 2w keys: 17 halves instead of the 18
+// of nine whole blocks when w = 256).  The softmax denominator is accumulated on the
+// VALU by v_dot2_f32_bf16 of the same bf16 probabilities that multiply V (per lane over
+// the lane's keys, summed over the row's four lanes at the end), which replaces the
+// all-ones MFMAs.
+template <typename OT, bool MASK, bool BUF>
+__global__ __launch_bounds__(256, MASK ? 3 : 5) void band_fused_half_kernel(BandGeom g, int ntx,
+                                                                 const bf16_t* __restrict__ Q,
+                                                                 const bf16_t* __restrict__ K,
+                                                                 const bf16_t* __restrict__ V,
+                                                                 OT* __restrict__ O) {
+    constexpr float kLazy = 64.f;
+    constexpr int NW = 4, HQ = 2, kSlots = 2;
+    constexpr int kQW = 16 * HQ;          // queries per wave
+    constexpr int kFT = NW * kQW;         // queries per tile
+    constexpr int kPass = 64 / (NW * 8);  // copy instructions per lane per 64-row block
+    __shared__ u32x4 lds[kSlots * kSlotChunks];
+    Tile t;
+    {
+        const int nblk_all = gridDim.x;
+        const int bid = blockIdx.x;
+        const int id = (nblk_all & 7) == 0 ? (bid & 7) * (nblk_all >> 3) + (bid >> 3) : bid;
+        t.q0 = (id % ntx) * kFT;
+        const int r = id / ntx;
+        t.rho = r % g.dil;
+        t.b = r / g.dil;
+        t.lr = ((int)g.l - t.rho + g.dil - 1) / g.dil;
+        if (t.q0 >= t.lr) return;
+    }
+    const int lane = threadIdx.x & 63, grp = lane >> 4, li = lane & 15;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int w = (int)g.w;
+    const int qa = t.q0 + wv * kQW;
+    const int xor16 = (lane ^ 16) << 2, xor32 = (lane ^ 32) << 2;
+    const float sl2 = fmaxf(fabsf(g.scale) * 1.4426950408889634f, 1.17549435e-38f);
+    const uint32_t qflip = g.scale < 0.f ? 0x80008000u : 0u;
+
+    bf16x8 qf[HQ][2];
+#pragma unroll
+    for (int hq = 0; hq < HQ; ++hq) {
+        const int q = qa + hq * 16 + li;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (q < t.lr)
+                v = *reinterpret_cast<const u32x4*>(Q + row_off(g, t, q) + kk * 32 + grp * 8);
+            v ^= (u32x4){qflip, qflip, qflip, qflip};
+            qf[hq][kk] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    const int nblk = (kFT + 2 * w + kT - 1) / kT;
+
+    const int dr = wv * 8 + (lane >> 3);
+    const int dch = (lane & 7) ^ ((lane >> 3) & 7);
+    const int64_t seq0 = ((int64_t)t.b * g.l + t.rho) * kD;
+    const char* kseq = reinterpret_cast<const char*>(K + seq0);
+    const char* vseq = reinterpret_cast<const char*>(V + seq0);
+    const uint32_t row_bytes = (uint32_t)g.dil * kD * 2;
+    const char* zero = reinterpret_cast<const char*>(kBandZero);
+    const int tt0 = t.q0 - w + dr;
+    const int nrec = BUF ? (t.lr - 1) * (int)row_bytes + kD * 2 : 0;
+    const int voff0 = BUF ? tt0 * (int)row_bytes + dch * 16 : 0;
+    auto dma = [&](int kb) {
+        u32x4* slot = lds + (kb % kSlots) * kSlotChunks;
+        if constexpr (BUF) {
+#pragma unroll
+            for (int e = 0; e < kPass; ++e) {
+                const uint32_t o2 = (uint32_t)(voff0 + (kb * kT + e * NW * 8) * (int)row_bytes);
+                buffer_copy16(kseq, nrec, o2, 0, (lds_void*)(slot + (e * NW + wv) * 64));
+                buffer_copy16(vseq, nrec, o2, 0, (lds_void*)(slot + 512 + (e * NW + wv) * 64));
+            }
+            return;
+        }
+        const int tt = tt0 + kb * kT;
+        if (t.q0 - w + kb * kT >= 0 && t.q0 - w + kb * kT + kT <= t.lr) {
+            const int64_t off = (int64_t)tt * row_bytes + dch * 16;
+#pragma unroll
+            for (int e = 0; e < kPass; ++e) {
+                const int64_t o2 = off + (int64_t)(e * NW * 8) * row_bytes;
+                __builtin_amdgcn_global_load_lds((const void*)(kseq + o2),
+                                                 (lds_void*)(slot + (e * NW + wv) * 64), 16, 0,
+                                                 0);
+                __builtin_amdgcn_global_load_lds((const void*)(vseq + o2),
+                                                 (lds_void*)(slot + 512 + (e * NW + wv) * 64),
+                                                 16, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < kPass; ++e) {
+                const int te = tt + NW * 8 * e;
+                const bool ok = te >= 0 && te < t.lr;
+                const int64_t o2 = (int64_t)te * row_bytes + dch * 16;
+                __builtin_amdgcn_global_load_lds((const void*)(ok ? kseq + o2 : zero),
+                                                 (lds_void*)(slot + (e * NW + wv) * 64), 16, 0,
+                                                 0);
+                __builtin_amdgcn_global_load_lds((const void*)(ok ? vseq + o2 : zero),
+                                                 (lds_void*)(slot + 512 + (e * NW + wv) * 64),
+                                                 16, 0, 0);
+            }
+        }
+    };
+    int koff[2], voff[4];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) koff[kk] = (li * 8 + ((4 * kk + grp) ^ (li & 7))) * 16;
+    {
+        const int vr = 4 * grp + (li >> 2);
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb)
+            voff[eb] = kT * 8 * 16 + (vr * 8 + ((2 * eb + ((li >> 1) & 1)) ^ (vr & 7))) * 16 +
+                       8 * (li & 1);
+    }
+    const char* lds_b = reinterpret_cast<const char*>(lds);
+    const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)lds;
+    auto wait_blocks = [](int later) {
+        constexpr int kC = 2 * kPass;
+        if (later >= 1) wait_vmcnt<kC>();
+        else wait_vmcnt<0>();
+    };
+
+    f32x4 o[HQ][4];
+    float lsum[HQ], m_run[HQ];
+#pragma unroll
+    for (int hq = 0; hq < HQ; ++hq) {
+        lsum[hq] = 0.f;
+        m_run[hq] = -INFINITY;
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb) o[hq][eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
+
+    // One 32-key half h of block kb: keys t0 + 32h + 16f + 4grp + v (f, v in 0..3/0..1)
+    auto half = [&](int kb, int h) {
+        const int t0 = t.q0 - w + kb * kT;
+        const int th = t0 + 32 * h;
+        f32x4 s[HQ][2];
+        {
+            const char* sb = lds_b + (kb % kSlots) * kSlotChunks * 16 + h * 32 * 128;
+#pragma unroll
+            for (int f = 0; f < 2; ++f) {
+                const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(sb + koff[0] + f * 16 * 128);
+                const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(sb + koff[1] + f * 16 * 128);
+#pragma unroll
+                for (int hq = 0; hq < HQ; ++hq) {
+                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qf[hq][0], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qf[hq][1], acc, 0, 0, 0);
+                    s[hq][f] = acc;
+                }
+            }
+        }
+        bool full = th >= qa + kQW - 1 - w && th + 31 <= qa + w;
+        if (MASK) full = full && th >= 0 && th + 32 <= t.lr;
+        if (!full) {
+#pragma unroll
+            for (int hq = 0; hq < HQ; ++hq) {
+                const int base = th + 4 * grp - (qa + hq * 16 + li) + w;
+#pragma unroll
+                for (int f = 0; f < 2; ++f)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        bool ok = (unsigned)(base + f * 16 + v) <= (unsigned)(2 * w);
+                        if (MASK) {
+                            const int tt = th + f * 16 + 4 * grp + v;
+                            ok = ok && tt >= 0 && tt < t.lr;
+                        }
+                        s[hq][f][v] = ok ? s[hq][f][v] : -INFINITY;
+                    }
+            }
+        }
+        float mb[HQ];
+#pragma unroll
+        for (int hq = 0; hq < HQ; ++hq) {
+            mb[hq] = -INFINITY;
+#pragma unroll
+            for (int f = 0; f < 2; ++f)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) mb[hq] = fmaxf(mb[hq], s[hq][f][v]);
+        }
+        bool up = false;
+#pragma unroll
+        for (int hq = 0; hq < HQ; ++hq) up = up || mb[hq] * sl2 > m_run[hq] + kLazy;
+        if (__any(up)) {
+#pragma unroll
+            for (int hq = 0; hq < HQ; ++hq) {
+                float m = mb[hq];
+                m = fmaxf(m, __int_as_float(__builtin_amdgcn_ds_bpermute(xor16, __float_as_int(m))));
+                m = fmaxf(m, __int_as_float(__builtin_amdgcn_ds_bpermute(xor32, __float_as_int(m))));
+                const float mbx = m * sl2;
+                const float m_new = mbx > m_run[hq] + kLazy ? mbx : m_run[hq];
+                const float corr =
+                    m_new == m_run[hq] ? 1.f : __builtin_amdgcn_exp2f(m_run[hq] - m_new);
+                lsum[hq] *= corr;
+#pragma unroll
+                for (int eb = 0; eb < 4; ++eb) o[hq][eb] *= corr;
+                m_run[hq] = m_new;
+            }
+        }
+        bf16x8 pf[HQ];
+#pragma unroll
+        for (int hq = 0; hq < HQ; ++hq) {
+            const float nm = m_run[hq] == -INFINITY ? 0.f : -m_run[hq];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                pf[hq][v] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][0][v], sl2, nm));
+                pf[hq][4 + v] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[hq][1][v], sl2, nm));
+            }
+            // (pairs formed from the elements: a bit_cast of the vector's dword e to a
+            // bf16 pair was compiled as dword 0 for every e)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bf16x2 pr = {pf[hq][2 * e], pf[hq][2 * e + 1]};
+                lsum[hq] = __builtin_amdgcn_fdot2_f32_bf16(pr, ones2, lsum[hq], false);
+            }
+        }
+        const uint32_t a0 = lds_a + (kb % kSlots) * kSlotChunks * 16 + h * 32 * 128;
+        bf16x8 vf[4];
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb) {
+            const uint32_t a = a0 + voff[eb];
+            s16x4 r[2] = {tr_read_raw<0>(a), tr_read_raw<16 * 128>(a)};
+            vf[eb] = __builtin_bit_cast(bf16x8, r);
+        }
+        lds_wait(vf);
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb)
+#pragma unroll
+            for (int hq = 0; hq < HQ; ++hq)
+                o[hq][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[eb], pf[hq], o[hq][eb], 0,
+                                                                    0, 0);
+    };
+    // the wave's band spans keys qa - w .. qa + kQW - 1 + w (subsequence indices)
+    const int klo = qa - w, khi = qa + kQW - 1 + w;
+#pragma unroll
+    for (int b = 0; b < kSlots - 1; ++b)
+        if (b < nblk) dma(b);
+    wait_blocks(min(nblk - 1, kSlots - 2));
+    block_sync();
+    for (int kb = 0; kb < nblk; ++kb) {
+        if (kb + kSlots - 1 < nblk) dma(kb + kSlots - 1);
+        const int t0 = t.q0 - w + kb * kT;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            if (t0 + 32 * h + 31 >= klo && t0 + 32 * h <= khi) half(kb, h);
+        wait_blocks(min(nblk - 1, kb + kSlots - 1) - (kb + 1));
+        block_sync();
+    }
+#pragma unroll
+    for (int hq = 0; hq < HQ; ++hq) {
+        float tot = lsum[hq];
+        tot += __int_as_float(__builtin_amdgcn_ds_bpermute(xor16, __float_as_int(tot)));
+        tot += __int_as_float(__builtin_amdgcn_ds_bpermute(xor32, __float_as_int(tot)));
+        const int q = qa + hq * 16 + li;
+        if (q >= t.lr) continue;
+        const float inv = 1.f / tot;
+        OT* orow = O + row_off(g, t, q);
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb) Out<OT>::put4(orow + eb * 16 + 4 * grp, o[hq][eb] * inv);
+    }
+}
+
 struct Grid {
     dim3 grid;
     int ntx;
@@ -746,14 +1014,40 @@ hipError_t launch_fused_nw(const BandGeom& g, const void* q, const void* k, cons
     return hipGetLastError();
 }
 
+hipError_t launch_fused_half(const BandGeom& g, const void* q, const void* k, const void* v,
+                             void* o, int o_bf16, int mask, hipStream_t stream) {
+    const int64_t l0 = (g.l + g.dil - 1) / g.dil;
+    const int ntx = (int)((l0 + 127) / 128);
+    const dim3 grid((unsigned)(ntx * g.dil * g.b));
+    const bool buf = (l0 + g.w + 4 * kT) * g.dil * kD * 2 < (int64_t(1) << 31);
+#define OLLIE_HALF(OT, M, B)                                                                 \
+    hipLaunchKernelGGL((band_fused_half_kernel<OT, M, B>), grid, dim3(256), 0, stream, g, ntx, \
+                       (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (OT*)o)
+#define OLLIE_HALF_B(OT, M)            \
+    if (buf) OLLIE_HALF(OT, M, true);  \
+    else OLLIE_HALF(OT, M, false)
+    if (o_bf16) {
+        if (mask) OLLIE_HALF_B(bf16_t, true);
+        else OLLIE_HALF_B(bf16_t, false);
+    } else {
+        if (mask) OLLIE_HALF_B(float, true);
+        else OLLIE_HALF_B(float, false);
+    }
+#undef OLLIE_HALF_B
+#undef OLLIE_HALF
+    return hipGetLastError();
+}
+
 // Wave shapes: 0 = four waves of 32 queries (the default: measured faster than eight
 // waves, which have half the copies per query but the same occupancy and twice the LDS
 // per workgroup), 1 = four waves of 64 queries, 2 = two waves of 64 queries (half the
-// LDS reads per score, two waves per SIMD).  `shape` (0..2, from the caller's flags;
-// -1 = automatic) overrides the choice for tuning sweeps and tests.
+// LDS reads per score, two waves per SIMD), 3 = four waves of 32 queries over 32-key
+// halves (band_fused_half_kernel).  `shape` (0..3, from the caller's flags; -1 =
+// automatic) overrides the choice for tuning sweeps and tests.
 hipError_t launch_band_fused(const BandGeom& g, const void* q, const void* k, const void* v,
                              void* o, int o_bf16, int mask, int shape, hipStream_t stream) {
     const int cfg = shape < 0 ? 0 : shape;
+    if (cfg == 3) return launch_fused_half(g, q, k, v, o, o_bf16, mask, stream);
     if (cfg == 1) return launch_fused_nw<4, 4>(g, q, k, v, o, o_bf16, mask, stream);
     if (cfg == 2) return launch_fused_nw<2, 4>(g, q, k, v, o, o_bf16, mask, stream);
     return launch_fused_nw<4, 2>(g, q, k, v, o, o_bf16, mask, stream);

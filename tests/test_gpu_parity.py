@@ -580,13 +580,13 @@ def test_band_small(ci, mask, staged, out_dtype):
     assert o.dtype == out_dtype
 
 
-# Every wave shape of the fused band kernel (flag bits BAND_SHAPE(0..2)): 32
+# Every wave shape of the fused band kernel (flag bits BAND_SHAPE(0..3)): 32
 # or 64 queries per wave, four or two waves per workgroup, on the small cases and
 # sequences long enough for several workgroups per residue subsequence (in the last,
 # the second tile of every odd residue lies past its subsequence).
 @pytest.mark.parametrize("ci", range(len(BAND_SMALL) + 4))
 @pytest.mark.parametrize("mask", [False, True])
-@pytest.mark.parametrize("cfg", [0, 1, 2])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
 def test_band_every_wave_shape(cfg, mask, ci):
     extra = [(2, 1100, 96, 2), (48, 2000, 64, 3), (64, 2600, 40, 1), (300, 257, 16, 2)]
     b, l, w, dil = BAND_SMALL[ci] if ci < len(BAND_SMALL) else extra[ci - len(BAND_SMALL)]
