@@ -46,7 +46,7 @@ def GEMM_TILE(n: int) -> int:
 
 
 def BAND_SHAPE(n: int) -> int:
-    """Flag bits forcing wave shape n (0..2) of the fused band kernel."""
+    """Flag bits forcing wave shape n (0..3) of the fused band kernel."""
     return ((n + 1) & 0xff) << 16
 
 

@@ -144,49 +144,34 @@ __device__ __forceinline__ s16x4 tr_read(const bf16_t* p) {
         (__attribute__((address_space(3))) s16x4*)(p));
 }
 
-// o[eb] (rows e = 16*eb + 4*grp + v, column = the lane's query) += V^T * P^T over the
-// block's 64 keys; p[ft][v] is the lane's probability for key 16*ft + 4*grp + v.
-__device__ __forceinline__ void pv_block(const bf16_t* lv, const f32x4 p[4], f32x4 o[4]) {
-    const int lane = threadIdx.x & 63;
-    const int grp = lane >> 4;
-    const int li = lane & 15;
-    const int col = 4 * (li & 3);      // this lane addresses a 4-column slice ...
-    const int krow = li >> 2;          // ... of key row 32h + 4*grp + krow (+16)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        bf16x8 pf;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            pf[v] = (__bf16)p[2 * h][v];
-            pf[4 + v] = (__bf16)p[2 * h + 1][v];
-        }
-        const bf16_t* base = lv + (32 * h + 4 * grp + krow) * kVLd + col;
-#pragma unroll
-        for (int eb = 0; eb < 4; ++eb) {
-            s16x4 lo = tr_read(base + eb * 16);
-            s16x4 hi = tr_read(base + 16 * kVLd + eb * 16);
-            s16x4 both[2] = {lo, hi};
-            bf16x8 vf = __builtin_bit_cast(bf16x8, both);
-            o[eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[eb], 0, 0, 0);
-        }
-    }
-}
-
 __device__ __forceinline__ int n_key_blocks(const BandGeom& g) {
     return (kT + 2 * (int)g.w + kT - 1) / kT;
 }
 
+// Ordering of one wave's accesses to its own LDS patch: a wave's LDS instructions
+// complete in issue order, so the compiler only has to keep them in program order.
+__device__ __forceinline__ void wave_lds_order() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+}
+
 // --------------------------------------------------------------------- G2BMM
-// Each wave owns 16 queries.  A block's 16 x 64 scores go through LDS so that they leave
-// row by row: for one query the block's 64 keys are 64 consecutive band entries of its
-// S row (j = key - query + w), written by the 64 lanes as one contiguous segment.
-constexpr int kPatchLd = kT + 4;   // fp32 row stride of a wave's score patch in LDS
+// Each wave owns 16 queries.  For one query a key block's 64 scores are 64 consecutive
+// band entries j = key - query + w of its S row, i.e. one run [a, a + 64) of S (a row
+// base plus the block's first j); runs of different rows start at any 4-byte offset.
+// The scores pass through a per-wave LDS patch so that S is written in aligned 16-byte
+// chunks: at a block the wave stores the 16 chunks of each row starting at a rounded
+// down to a multiple of 4.  The first chunk's entries below a came from the previous
+// block (kept in the patch's 4-entry carry), the entries above the last chunk leave
+// with the next block (or the final flush).  Chunks that reach past a row's ends
+// [0, 2w] are stored entry by entry, the rest as one 16-byte store each: every
+// instruction writes four 256-byte runs.
+constexpr int kSLd = kT + 4;   // patch row: 4 carried scores, then the block's 64
 __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
                                                         const bf16_t* __restrict__ Q,
                                                         const bf16_t* __restrict__ K,
                                                         float* __restrict__ S) {
     __shared__ u32x4 lk[kT * 8];
-    __shared__ __attribute__((aligned(16))) float ls[4][16 * kPatchLd];
+    __shared__ __attribute__((aligned(16))) float ls[4][16 * kSLd];
     Tile t;
     if (!tile_of(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
@@ -196,6 +181,14 @@ __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
     load_q_frags(g, t, Q, qw + (lane & 15), qf);
     const int nblk = n_key_blocks(g);
     float* patch = ls[wv];
+    // chunk-store slots: instruction n, lane -> row rr = 4n + lane/16, chunk c = lane%16
+    const int cc = lane & 15;
+    int64_t rbase[4];                               // S offset of row rr (-1: no row)
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+        const int qq = qw + 4 * n + (lane >> 4);
+        rbase[n] = qq < t.lr ? row_index(g, t, qq) * nb : -1;
+    }
     KVRegs r;
     gload_block<true, false>(g, t, K, nullptr, t.q0 - w, r);
     for (int kb = 0; kb < nblk; ++kb) {
@@ -203,22 +196,49 @@ __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
         __syncthreads();
         lstore_block<true, false>(r, lk, nullptr);
         __syncthreads();
-        // the next key block's loads overlap this block's scores and row stores
+        // the next key block's loads overlap this block's scores and stores
         if (kb + 1 < nblk) gload_block<true, false>(g, t, K, nullptr, t0 + kT, r);
         f32x4 s[4];
         score_block(lk, qf, s);
 #pragma unroll
         for (int ft = 0; ft < 4; ++ft)   // query lane%16, keys 16ft + 4grp .. +3
-            *reinterpret_cast<f32x4*>(patch + (lane & 15) * kPatchLd + ft * 16 + 4 * grp) =
+            *reinterpret_cast<f32x4*>(patch + (lane & 15) * kSLd + 4 + ft * 16 + 4 * grp) =
                 s[ft] * g.scale;
-        __syncthreads();
-#pragma unroll 4
-        for (int rr = 0; rr < 16; ++rr) {
-            const int qq = qw + rr;
-            const int j = t0 + lane - qq + w;    // lane = key offset in the block
-            if (qq < t.lr && j >= 0 && j < nb)
-                S[row_index(g, t, qq) * nb + j] = patch[rr * kPatchLd + lane];
+        wave_lds_order();
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+            if (rbase[n] < 0) continue;
+            const int rr = 4 * n + (lane >> 4);
+            const int js = t0 - (qw + rr) + w;      // j of the block's first key
+            const int64_t a = rbase[n] + js;
+            const int64_t x0 = (a & ~int64_t(3)) + 4 * cc;
+            const int j0 = (int)(x0 - rbase[n]);
+            const float* src = patch + rr * kSLd + 4 + (int)(x0 - a);
+            if (j0 >= 0 && j0 + 3 < nb) {
+                const f32x4 v = {src[0], src[1], src[2], src[3]};
+                *reinterpret_cast<f32x4*>(S + x0) = v;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (j0 + e >= 0 && j0 + e < nb) S[x0 + e] = src[e];
+            }
         }
+        wave_lds_order();
+        // carry: the block's last 4 scores of each row (lane -> row lane/4, entry lane%4)
+        patch[(lane >> 2) * kSLd + (lane & 3)] = patch[(lane >> 2) * kSLd + kT + (lane & 3)];
+        wave_lds_order();
+    }
+    // flush: the entries of the last block above its last stored chunk (lane -> row
+    // lane/4, entry lane%4 of the chunk after it)
+    const int rr = lane >> 2;
+    const int qq = qw + rr;
+    if (qq < t.lr) {
+        const int64_t rb = row_index(g, t, qq) * nb;
+        const int js = t.q0 - w + (nblk - 1) * kT - qq + w;
+        const int64_t a = rb + js;
+        const int64_t x = (a & ~int64_t(3)) + kT + (lane & 3);
+        const int j = (int)(x - rb);
+        if (x < a + kT && j >= 0 && j < nb) S[x] = patch[rr * kSLd + 4 + (int)(x - a)];
     }
 }
 
@@ -270,54 +290,124 @@ __global__ __launch_bounds__(256) void band_softmax_kernel(BandGeom g, const flo
 }
 
 // ---------------------------------------------------------------------- GBMM
-// The probabilities of a block arrive the same way the scores leave the G2BMM: row by
-// row, the 64 lanes reading one query's 64 consecutive band entries, through a per-wave
-// LDS patch from which each lane takes its MFMA operand.
-constexpr int kPLd = kT + 8;   // bf16 row stride of a wave's probability patch in LDS
+// The probabilities of a block come in the way the G2BMM's scores leave: for one query
+// the block's 64 keys are the run [a, a + 64) of its P row, fetched as aligned 16-byte
+// chunks (8 entries) into a per-wave LDS patch.  Slot 0 of a patch row holds the chunk
+// containing a (the previous block's last chunk, carried), slots 1..8 the next eight
+// chunks, loaded for this block during the previous one: every load instruction reads
+// eight 128-byte runs.  Entries outside the row [0, 2w] enter the patch as zeros.  A
+// lane then takes its MFMA operand, the four entries at a + 32h + 16f + 4grp .. +3, from
+// three patch dwords shifted by 0 or 16 bits.
+constexpr int kPSlots = 9;   // 16-byte slots per patch row
+
+// Entries [x0, x0 + 8) of the P row based at rb (zero outside [0, nb)).
+__device__ __forceinline__ u32x4 load_p_chunk(const bf16_t* __restrict__ P, int64_t rb,
+                                              int64_t x0, int nb) {
+    const int j0 = (int)(x0 - rb);
+    if (j0 >= 0 && j0 + 7 < nb) return *reinterpret_cast<const u32x4*>(P + x0);
+    uint32_t e[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) e[v] = (j0 + v >= 0 && j0 + v < nb) ? (uint32_t)P[x0 + v] : 0u;
+    return (u32x4){e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                   e[6] | (e[7] << 16)};
+}
+
 template <typename OT>
 __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
                                                        const bf16_t* __restrict__ P,
                                                        const bf16_t* __restrict__ V,
                                                        OT* __restrict__ O) {
+    constexpr int kRows = 16;                       // P rows (queries) per wave
+    constexpr int kLoads = kRows * 8 / 64;          // chunk loads per lane per block
     __shared__ __attribute__((aligned(16))) bf16_t lv[kT * kVLd];
-    __shared__ __attribute__((aligned(16))) bf16_t lp[4][16 * kPLd];
+    __shared__ u32x4 lp[4][kRows * kPSlots];
     Tile t;
     if (!tile_of(g, ntx, t)) return;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
-    const int qw = t.q0 + wv * 16;
-    const int q = qw + (lane & 15);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4, li = lane & 15;
+    const int qw = t.q0 + wv * kRows;
     const int w = (int)g.w, nb = 2 * w + 1;
     const int nblk = n_key_blocks(g);
-    bf16_t* patch = lp[wv];
+    u32x4* patch = lp[wv];
+    // chunk-load slots: instruction n, lane -> row rr = 8n + lane/8, chunk c = lane%8
+    const int cc = lane & 7;
+    int64_t rbase[kLoads];                          // P offset of row rr (-1: no row)
+#pragma unroll
+    for (int n = 0; n < kLoads; ++n) {
+        const int qq = qw + 8 * n + (lane >> 3);
+        rbase[n] = qq < t.lr ? row_index(g, t, qq) * nb : -1;
+    }
+    // aligned start of block kb's run for slot row rr (the chunk in slot 0)
+    auto chunk0 = [&](int n, int kb) -> int64_t {
+        const int rr = 8 * n + (lane >> 3);
+        const int js = t.q0 - w + kb * kT - (qw + rr) + w;
+        return (rbase[n] + js) & ~int64_t(7);
+    };
+    // slots 1..8 of block kb
+    auto load_p = [&](int kb, u32x4 (&pc)[kLoads]) {
+#pragma unroll
+        for (int n = 0; n < kLoads; ++n)
+            pc[n] = rbase[n] < 0 ? (u32x4){0u, 0u, 0u, 0u}
+                                 : load_p_chunk(P, rbase[n], chunk0(n, kb) + 8 + 8 * cc, nb);
+    };
+    // slot 0 of block 0 (lanes with chunk index 0 of each row)
+    if (cc == 0) {
+#pragma unroll
+        for (int n = 0; n < kLoads; ++n)
+            patch[(8 * n + (lane >> 3)) * kPSlots] =
+                rbase[n] < 0 ? (u32x4){0u, 0u, 0u, 0u}
+                             : load_p_chunk(P, rbase[n], chunk0(n, 0), nb);
+    }
+    // the lane's operand offset in its patch row: a - chunk0 (0..7) in entries
+    const int q = qw + li;
+    const int64_t ra = q < t.lr ? row_index(g, t, q) * nb + (t.q0 - w) - q + w : 0;
+    const int o0 = (int)(ra & 7);
+    const int col = 4 * (li & 3), krow = li >> 2;
     f32x4 o[4];
 #pragma unroll
     for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
     KVRegs r;
+    u32x4 pc[kLoads];
     gload_block<false, true>(g, t, nullptr, V, t.q0 - w, r);
+    load_p(0, pc);
+    const uint32_t* prow = reinterpret_cast<const uint32_t*>(patch + li * kPSlots);
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
-#pragma unroll 4
-        for (int rr = 0; rr < 16; ++rr) {
-            const int qq = qw + rr;
-            const int j = t0 + lane - qq + w;
-            bf16_t val = 0;
-            if (qq < t.lr && j >= 0 && j < nb) val = P[row_index(g, t, qq) * nb + j];
-            patch[rr * kPLd + lane] = val;
-        }
         __syncthreads();
         lstore_block<false, true>(r, nullptr, lv);
-        __syncthreads();
-        // the next value block's loads overlap this block's products
-        if (kb + 1 < nblk) gload_block<false, true>(g, t, nullptr, V, t0 + kT, r);
-        f32x4 p[4];
 #pragma unroll
-        for (int ft = 0; ft < 4; ++ft) {   // keys 16ft + 4grp .. +3 of query lane%16
-            const uint2 u = *reinterpret_cast<const uint2*>(patch + (lane & 15) * kPLd +
-                                                            ft * 16 + 4 * grp);
-            p[ft] = (f32x4){__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
-                            __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+        for (int n = 0; n < kLoads; ++n) patch[(8 * n + (lane >> 3)) * kPSlots + 1 + cc] = pc[n];
+        __syncthreads();
+        // the next block's value and probability loads overlap this block's products
+        if (kb + 1 < nblk) {
+            gload_block<false, true>(g, t, nullptr, V, t0 + kT, r);
+            load_p(kb + 1, pc);
         }
-        pv_block(lv, p, o);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t pu[4];
+#pragma unroll
+            for (int f = 0; f < 2; ++f) {
+                const int e = o0 + 32 * h + 16 * f + 4 * grp;   // patch entry of the run
+                const int d = e >> 1, sh = (e & 1) * 16;
+                const uint32_t d0 = prow[d], d1 = prow[d + 1], d2 = prow[d + 2];
+                pu[2 * f] = __builtin_amdgcn_alignbit(d1, d0, sh);
+                pu[2 * f + 1] = __builtin_amdgcn_alignbit(d2, d1, sh);
+            }
+            const u32x4 pv = {pu[0], pu[1], pu[2], pu[3]};
+            const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
+            const bf16_t* base = lv + (32 * h + 4 * grp + krow) * kVLd + col;
+#pragma unroll
+            for (int eb = 0; eb < 4; ++eb) {
+                s16x4 lo = tr_read(base + eb * 16);
+                s16x4 hi = tr_read(base + 16 * kVLd + eb * 16);
+                s16x4 both[2] = {lo, hi};
+                bf16x8 vf = __builtin_bit_cast(bf16x8, both);
+                o[eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[eb], 0, 0, 0);
+            }
+        }
+        wave_lds_order();
+        // carry: slot 8 becomes the next block's slot 0 (one lane per row)
+        if (lane < kRows) patch[lane * kPSlots] = patch[lane * kPSlots + 8];
     }
     if (q >= t.lr) return;
     OT* orow = O + row_off(g, t, q);

@@ -331,7 +331,7 @@ def test_tile_override_bits(lib):
     def bcall(flags, ws_bytes=0):
         return lib.banded_bmm(ctypes.byref(bd), A16, B16, C16, W16, None, WSB, ws_bytes,
                               flags, None)
-    assert bcall(ol.BAND_SHAPE(3)) == ol.EINVAL
+    assert bcall(ol.BAND_SHAPE(4)) == ol.EINVAL
     assert bcall(ol.BAND_STAGED | ol.BAND_SHAPE(2), ws_bytes=8) == ol.EWORKSPACE
     assert bcall(ol.GEMM_TILE(0)) == ol.EINVAL                # not a band flag
 
