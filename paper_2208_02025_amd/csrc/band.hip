@@ -46,11 +46,12 @@ struct Tile {
 // Tiles are numbered (tile, residue, batch) with the tile fastest.  Workgroup ids are
 // dealt round-robin to the 8 XCDs; remap them so each XCD owns a contiguous run of
 // tiles of the same sequences, whose key/value blocks then stay in that XCD's L2.
+template <int FT = kT>   // queries per tile
 __device__ __forceinline__ bool tile_of(const BandGeom& g, int ntx, Tile& t) {
     const int nblk = gridDim.x;
     const int bid = blockIdx.x;
     const int id = (nblk & 7) == 0 ? (bid & 7) * (nblk >> 3) + (bid >> 3) : bid;
-    t.q0 = (id % ntx) * kT;
+    t.q0 = (id % ntx) * FT;
     const int r = id / ntx;
     t.rho = r % g.dil;
     t.b = r / g.dil;
@@ -69,19 +70,21 @@ __device__ __forceinline__ int64_t row_off(const BandGeom& g, const Tile& t, int
 
 __device__ __forceinline__ int kswz(int row, int ch) { return row * 8 + (ch ^ (row & 7)); }
 
-// Register staging of one 64-row block of K (and V): 2 x 16 bytes per thread each.
+// Register staging of one 64-row block of K (and V), 512 16-byte chunks each: 2 per
+// thread of a 256-thread workgroup (NT = 256), 1 per thread of a 512-thread one.
 struct KVRegs {
     u32x4 k[2];
     u32x4 v[2];
 };
 
-template <bool WITH_K, bool WITH_V>
+template <bool WITH_K, bool WITH_V, int NT = 256>
 __device__ __forceinline__ void gload_block(const BandGeom& g, const Tile& t,
                                             const bf16_t* __restrict__ K,
                                             const bf16_t* __restrict__ V, int t0, KVRegs& r) {
+    static_assert(NT == 256 || NT == 512, "workgroup size");
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-        const int idx = threadIdx.x + e * 256;
+    for (int e = 0; e < 512 / NT; ++e) {
+        const int idx = threadIdx.x + e * NT;
         const int row = idx >> 3, ch = idx & 7;
         const int tt = t0 + row;
         u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
@@ -97,11 +100,11 @@ __device__ __forceinline__ void gload_block(const BandGeom& g, const Tile& t,
 
 // K block: 16-byte chunks with an XOR swizzle (conflict-free ds_read_b128 fragments).
 // V block: plain rows padded to kVLd elements (read through the transposing load).
-template <bool WITH_K, bool WITH_V>
+template <bool WITH_K, bool WITH_V, int NT = 256>
 __device__ __forceinline__ void lstore_block(const KVRegs& r, u32x4* lk, bf16_t* lv) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-        const int idx = threadIdx.x + e * 256;
+    for (int e = 0; e < 512 / NT; ++e) {
+        const int idx = threadIdx.x + e * NT;
         const int row = idx >> 3, ch = idx & 7;
         if (WITH_K) lk[kswz(row, ch)] = r.k[e];
         if (WITH_V) *reinterpret_cast<u32x4*>(lv + row * kVLd + ch * 8) = r.v[e];
@@ -144,8 +147,9 @@ __device__ __forceinline__ s16x4 tr_read(const bf16_t* p) {
         (__attribute__((address_space(3))) s16x4*)(p));
 }
 
+template <int FT = kT>   // key blocks that meet the band of a tile of FT queries
 __device__ __forceinline__ int n_key_blocks(const BandGeom& g) {
-    return (kT + 2 * (int)g.w + kT - 1) / kT;
+    return (FT + 2 * (int)g.w + kT - 1) / kT;
 }
 
 // Ordering of one wave's accesses to its own LDS patch: a wave's LDS instructions
@@ -166,20 +170,22 @@ __device__ __forceinline__ void wave_lds_order() {
 // [0, 2w] are stored entry by entry, the rest as one 16-byte store each: every
 // instruction writes four 256-byte runs.
 constexpr int kSLd = kT + 4;   // patch row: 4 carried scores, then the block's 64
-__global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
-                                                        const bf16_t* __restrict__ Q,
-                                                        const bf16_t* __restrict__ K,
-                                                        float* __restrict__ S) {
+template <int NW>   // waves per workgroup: a tile of 16*NW queries
+__global__ __launch_bounds__(64 * NW) void band_g2bmm_kernel(BandGeom g, int ntx,
+                                                            const bf16_t* __restrict__ Q,
+                                                            const bf16_t* __restrict__ K,
+                                                            float* __restrict__ S) {
+    constexpr int NT = 64 * NW, FT = 16 * NW;
     __shared__ u32x4 lk[kT * 8];
-    __shared__ __attribute__((aligned(16))) float ls[4][16 * kSLd];
+    __shared__ __attribute__((aligned(16))) float ls[NW][16 * kSLd];
     Tile t;
-    if (!tile_of(g, ntx, t)) return;
+    if (!tile_of<FT>(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4;
     const int qw = t.q0 + wv * 16;                  // the wave's first query
     const int w = (int)g.w, nb = 2 * w + 1;
     bf16x8 qf[2];
     load_q_frags(g, t, Q, qw + (lane & 15), qf);
-    const int nblk = n_key_blocks(g);
+    const int nblk = n_key_blocks<FT>(g);
     float* patch = ls[wv];
     // chunk-store slots: instruction n, lane -> row rr = 4n + lane/16, chunk c = lane%16
     const int cc = lane & 15;
@@ -190,14 +196,14 @@ __global__ __launch_bounds__(256) void band_g2bmm_kernel(BandGeom g, int ntx,
         rbase[n] = qq < t.lr ? row_index(g, t, qq) * nb : -1;
     }
     KVRegs r;
-    gload_block<true, false>(g, t, K, nullptr, t.q0 - w, r);
+    gload_block<true, false, NT>(g, t, K, nullptr, t.q0 - w, r);
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
         __syncthreads();
-        lstore_block<true, false>(r, lk, nullptr);
+        lstore_block<true, false, NT>(r, lk, nullptr);
         __syncthreads();
         // the next key block's loads overlap this block's scores and stores
-        if (kb + 1 < nblk) gload_block<true, false>(g, t, K, nullptr, t0 + kT, r);
+        if (kb + 1 < nblk) gload_block<true, false, NT>(g, t, K, nullptr, t0 + kT, r);
         f32x4 s[4];
         score_block(lk, qf, s);
 #pragma unroll
@@ -312,21 +318,22 @@ __device__ __forceinline__ u32x4 load_p_chunk(const bf16_t* __restrict__ P, int6
                    e[6] | (e[7] << 16)};
 }
 
-template <typename OT>
-__global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
-                                                       const bf16_t* __restrict__ P,
-                                                       const bf16_t* __restrict__ V,
-                                                       OT* __restrict__ O) {
+template <typename OT, int NW>   // NW waves per workgroup: a tile of 16*NW queries
+__global__ __launch_bounds__(64 * NW) void band_gbmm_kernel(BandGeom g, int ntx,
+                                                           const bf16_t* __restrict__ P,
+                                                           const bf16_t* __restrict__ V,
+                                                           OT* __restrict__ O) {
+    constexpr int NT = 64 * NW, FT = 16 * NW;
     constexpr int kRows = 16;                       // P rows (queries) per wave
     constexpr int kLoads = kRows * 8 / 64;          // chunk loads per lane per block
     __shared__ __attribute__((aligned(16))) bf16_t lv[kT * kVLd];
-    __shared__ u32x4 lp[4][kRows * kPSlots];
+    __shared__ u32x4 lp[NW][kRows * kPSlots];
     Tile t;
-    if (!tile_of(g, ntx, t)) return;
+    if (!tile_of<FT>(g, ntx, t)) return;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, grp = lane >> 4, li = lane & 15;
     const int qw = t.q0 + wv * kRows;
     const int w = (int)g.w, nb = 2 * w + 1;
-    const int nblk = n_key_blocks(g);
+    const int nblk = n_key_blocks<FT>(g);
     u32x4* patch = lp[wv];
     // chunk-load slots: instruction n, lane -> row rr = 8n + lane/8, chunk c = lane%8
     const int cc = lane & 7;
@@ -367,19 +374,19 @@ __global__ __launch_bounds__(256) void band_gbmm_kernel(BandGeom g, int ntx,
     for (int eb = 0; eb < 4; ++eb) o[eb] = (f32x4){0.f, 0.f, 0.f, 0.f};
     KVRegs r;
     u32x4 pc[kLoads];
-    gload_block<false, true>(g, t, nullptr, V, t.q0 - w, r);
+    gload_block<false, true, NT>(g, t, nullptr, V, t.q0 - w, r);
     load_p(0, pc);
     const uint32_t* prow = reinterpret_cast<const uint32_t*>(patch + li * kPSlots);
     for (int kb = 0; kb < nblk; ++kb) {
         const int t0 = t.q0 - w + kb * kT;
         __syncthreads();
-        lstore_block<false, true>(r, nullptr, lv);
+        lstore_block<false, true, NT>(r, nullptr, lv);
 #pragma unroll
         for (int n = 0; n < kLoads; ++n) patch[(8 * n + (lane >> 3)) * kPSlots + 1 + cc] = pc[n];
         __syncthreads();
         // the next block's value and probability loads overlap this block's products
         if (kb + 1 < nblk) {
-            gload_block<false, true>(g, t, nullptr, V, t0 + kT, r);
+            gload_block<false, true, NT>(g, t, nullptr, V, t0 + kT, r);
             load_p(kb + 1, pc);
         }
 #pragma unroll
@@ -1031,9 +1038,15 @@ struct Grid {
     int ntx;
 };
 
-Grid tile_grid(const BandGeom& g) {
+// Waves per workgroup of the staged G2BMM and GBMM (tiles of 16 queries per wave).
+// Eight G2BMM waves share each key block (each key row is read by 5 tiles instead of
+// 9 at the Longformer band); the GBMM measured slower with eight.
+constexpr int kG2bmmWaves = 8;
+constexpr int kGbmmWaves = 4;
+
+Grid tile_grid(const BandGeom& g, int ft = kT) {
     const int64_t l0 = (g.l + g.dil - 1) / g.dil;   // longest residue subsequence (rho = 0)
-    const int ntx = (int)((l0 + kT - 1) / kT);
+    const int ntx = (int)((l0 + ft - 1) / ft);
     return {dim3((unsigned)(ntx * g.dil * g.b)), ntx};
 }
 
@@ -1041,8 +1054,9 @@ Grid tile_grid(const BandGeom& g) {
 
 hipError_t launch_band_g2bmm(const BandGeom& g, const void* q, const void* k, float* s,
                              hipStream_t stream) {
-    Grid gr = tile_grid(g);
-    hipLaunchKernelGGL(band_g2bmm_kernel, gr.grid, dim3(256), 0, stream, g, gr.ntx,
+    constexpr int NW = kG2bmmWaves;
+    Grid gr = tile_grid(g, 16 * NW);
+    hipLaunchKernelGGL(band_g2bmm_kernel<NW>, gr.grid, dim3(64 * NW), 0, stream, g, gr.ntx,
                        (const bf16_t*)q, (const bf16_t*)k, s);
     return hipGetLastError();
 }
@@ -1067,13 +1081,14 @@ hipError_t launch_band_softmax(const BandGeom& g, const float* s, void* p, int m
 
 hipError_t launch_band_gbmm(const BandGeom& g, const void* p, const void* v, void* o,
                             int o_bf16, hipStream_t stream) {
-    Grid gr = tile_grid(g);
+    constexpr int NW = kGbmmWaves;
+    Grid gr = tile_grid(g, 16 * NW);
     if (o_bf16)
-        hipLaunchKernelGGL(band_gbmm_kernel<bf16_t>, gr.grid, dim3(256), 0, stream, g, gr.ntx,
-                           (const bf16_t*)p, (const bf16_t*)v, (bf16_t*)o);
+        hipLaunchKernelGGL((band_gbmm_kernel<bf16_t, NW>), gr.grid, dim3(64 * NW), 0, stream, g,
+                           gr.ntx, (const bf16_t*)p, (const bf16_t*)v, (bf16_t*)o);
     else
-        hipLaunchKernelGGL(band_gbmm_kernel<float>, gr.grid, dim3(256), 0, stream, g, gr.ntx,
-                           (const bf16_t*)p, (const bf16_t*)v, (float*)o);
+        hipLaunchKernelGGL((band_gbmm_kernel<float, NW>), gr.grid, dim3(64 * NW), 0, stream, g,
+                           gr.ntx, (const bf16_t*)p, (const bf16_t*)v, (float*)o);
     return hipGetLastError();
 }
 
