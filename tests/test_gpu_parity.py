@@ -580,6 +580,34 @@ def test_band_small(ci, mask, staged, out_dtype):
     assert o.dtype == out_dtype
 
 
+# The staged G2BMM and GBMM move S and P rows (2w+1 entries, starting at any 4- or
+# 2-byte offset) as aligned 16-byte chunks, carrying the entries that straddle two key
+# blocks: the widest bands the staged softmax takes (2w+1 up to 1023), several tiles per
+# residue subsequence, S compared entry by entry and O through the staged path.
+BAND_WIDE = [(1, 700, 511, 1), (2, 600, 300, 3), (1, 1500, 257, 2)]
+
+
+@pytest.mark.parametrize("ci", range(len(BAND_WIDE)))
+@pytest.mark.parametrize("mask", [False, True])
+def test_band_staged_wide_bands(ci, mask):
+    b, l, w, dil = BAND_WIDE[ci]
+    say("band staged wide", BAND_WIDE[ci], "mask", mask)
+    q = synth.random_tensor((b, l, 64), 15000 + ci, "bf16", dist="normal")
+    k = synth.random_tensor((b, l, 64), 15100 + ci, "bf16", dist="normal")
+    v = synth.random_tensor((b, l, 64), 15200 + ci, "bf16", dist="normal")
+    o, sg = ol.banded_bmm(q.to(DEV), k.to(DEV), v.to(DEV), w, dil, 0.125, mask_invalid=mask,
+                          staged=True, return_s=True)
+    torch.cuda.synchronize()
+    s_ref, _, o_ref = oracle.band(q, k, v, w, dil, 0.125, mask, want_p=False)
+    sn = to_np(sg).reshape(s_ref.shape)
+    # S is a bf16 x bf16 dot product accumulated in fp32: exact up to rounding, and
+    # every entry outside [0, l) holds the zero-mode value 0 exactly
+    assert err(sn, s_ref) <= 1e-5
+    on = to_np(o).reshape(o_ref.shape)
+    assert np.isfinite(on).all()
+    assert err(on, o_ref) <= TOL_BF16
+
+
 # Every wave shape of the fused band kernel (flag bits BAND_SHAPE(0..3)): 32
 # or 64 queries per wave, four or two waves per workgroup, on the small cases and
 # sequences long enough for several workgroups per residue subsequence (in the last,
