@@ -694,19 +694,22 @@ def test_band_fused_and_staged_agree_at_full_size():
     assert d <= TOL_BF16
 
 
+@pytest.mark.parametrize("staged", [False, True])
 @pytest.mark.parametrize("mask", [False, True])
-def test_band_subsequence_over_4gib_sampled(mask):
+def test_band_subsequence_over_4gib_sampled(mask, staged):
     """A residue subsequence whose keys span more than 4 GiB takes the band kernel's
-    64-bit address form.  Sampled query rows (sequence ends, and keys on both sides of
-    the 2^31- and 2^32-byte offsets of the subsequence) match the oracle run on the
-    window of keys each row reaches (the same keys lie inside and outside [0, L), so
-    the same rows and zero/masked entries enter its softmax)."""
+    64-bit address form (and the staged kernels' 64-bit row offsets, S and P then
+    spanning 0.9 and 0.5 GB).  Sampled query rows (sequence ends, and keys on both
+    sides of the 2^31- and 2^32-byte offsets of the subsequence) match the oracle run
+    on the window of keys each row reaches (the same keys lie inside and outside
+    [0, L), so the same rows and zero/masked entries enter its softmax)."""
     b, l, w, dil, scale = 1, (1 << 25) + 4096, 3, 2, 0.05
-    say("band over 4 GiB", b, l, w, dil, "mask" if mask else "no mask")
+    say("band over 4 GiB", b, l, w, dil, "mask" if mask else "no mask",
+        "staged" if staged else "fused")
     q = synth.device_integer_tensor((b, l, 64), 6300, DEV)
     k = synth.device_integer_tensor((b, l, 64), 6301, DEV)
     v = synth.device_integer_tensor((b, l, 64), 6302, DEV)
-    o = ol.banded_bmm(q, k, v, w, dil, scale, mask_invalid=mask)
+    o = ol.banded_bmm(q, k, v, w, dil, scale, mask_invalid=mask, staged=staged)
     torch.cuda.synchronize()
     rng = np.random.default_rng(6303)
     rows = sorted(set([0, 1, 5, l - 1, l - 2, l - 7, (1 << 24) - 1, 1 << 24, (1 << 24) + 1,
