@@ -5,19 +5,21 @@
 // Dilation removal (section 6.4): with row i = dil*i' + rho the key of band entry j is
 //   t = i + (j - w)*dil = dil*(i' + j - w) + rho,
 // a NON-dilated band t' = i' + j - w on the residue-rho subsequence.  Every kernel
-// works on one (batch, residue, 64-query tile) of that subsequence, so keys and
-// values are read as contiguous 64-row blocks of the strided view (no copy is made).
+// works on one (batch, residue, query tile) of that subsequence (64 or 128 queries),
+// so keys and values are read as contiguous 64-row blocks of the strided view (no copy
+// is made).
 //
-// Work split inside a 256-thread workgroup: wave wv owns the 16 queries
-// q0 + 16*wv .. +15 and, for each 64-key block, computes the transposed score block
+// Work split: a wave owns one or more groups of 16 consecutive queries q0' .. q0' + 15
+// and, for each 64-key block, computes the transposed score block
 // S^T[t][q] = K[t] . Q[q] with v_mfma_f32_16x16x32_bf16 (A operand = key rows,
-// B operand = query rows).  Lane l then holds the scores of query q0+16*wv+l%16 for
+// B operand = query rows).  Lane l then holds the scores of query q0' + l%16 for
 // keys 16*ft + 4*(l/16) + v (ft, v in 0..3): every value of a lane belongs to one
 // query, so softmax statistics stay per lane until a final 4-lane reduction.
 //
 // For P*V the contraction runs over keys.  The MFMA's k-slots are assigned so that
 // lane group g = l/16 of a 32-key half h supplies keys 32h + {4g..4g+3, 16+4g..16+4g+3}:
-// exactly the keys the lane already holds in registers.  The V^T operand comes from a
+// in the fused kernel exactly the keys the lane already holds in registers (the staged
+// GBMM takes the same entries from its P rows).  The V^T operand comes from a
 // row-major LDS copy of the value block through ds_read_b64_tr_b16, whose lane i of
 // each 16-lane group receives element i%4 of the 8-byte rows addressed by lanes
 // i/4 + 4j (j = 0..3): lanes address rows (keys) and 4-column slices, the hardware
