@@ -8,6 +8,10 @@ Conv5x5 -> Conv3x3 split form (fused and two-stage 3x3 stage), the residue sub-i
 form of the dilated convolution and the allocation-free entry point.  With integer
 inputs every partial sum is an integer below 2^24, so each form must equal the oracle's
 convolution exactly.
+
+A second sweep draws banded problems (batch, length, half-width, dilation, zero or mask
+mode) and runs every wave shape of the fused kernel and the staged path against the
+oracle.
 """
 import sys
 
@@ -112,3 +116,53 @@ def test_random_shapes_every_form_integer_exact(ci):
         got = out.float().cpu().numpy()
         assert got.shape == ref.shape, name
         assert np.array_equal(got, ref), name
+
+
+def draw_band_cases(n_cases, seed):
+    """Random band problems: batch, length (several tiles and ragged tails, down to a
+    single row), half-width up to 300 (2w+1 within the staged softmax's 1024) and
+    dilation 1-5 (residues longer and shorter than a tile, or empty)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n_cases):
+        b = int(rng.integers(1, 5))
+        l = int(rng.choice([1, 2, 63, 64, 65, 129, int(rng.integers(3, 900))]))
+        w = int(rng.integers(0, 301))
+        dil = int(rng.integers(1, 6))
+        mask = bool(rng.integers(0, 2))
+        cases.append((b, l, w, dil, mask))
+    return cases
+
+
+BAND_CASES = draw_band_cases(40, 20240918)
+TOL_BF16 = 2e-2
+
+
+@pytest.mark.parametrize("ci", range(len(BAND_CASES)))
+def test_random_bands_every_path(ci):
+    """Every fused wave shape and the staged path on a random band problem: O against
+    the oracle within the bf16 bar, and the staged S (integer Q, K: exact in fp32)
+    entry by entry."""
+    b, l, w, dil, mask = BAND_CASES[ci]
+    scale = 0.0625   # a power of two: the scaled integer scores are exact in fp32
+    q = synth.random_tensor((b, l, 64), 32000 + ci, "bf16", integer=True)
+    k = synth.random_tensor((b, l, 64), 32100 + ci, "bf16", integer=True)
+    v = synth.random_tensor((b, l, 64), 32200 + ci, "bf16", dist="normal")
+    s_ref, _, o_ref = oracle.band(q, k, v, w, dil, scale, mask, want_p=False)
+    qg, kg, vg = q.to(DEV), k.to(DEV), v.to(DEV)
+    den = max(float(np.abs(o_ref).max()), 1e-30)
+    for shape in range(4):
+        say("band sweep", ci, BAND_CASES[ci], "shape", shape)
+        o = ol.banded_bmm(qg, kg, vg, w, dil, scale, mask_invalid=mask,
+                          flags=ol.BAND_SHAPE(shape))
+        torch.cuda.synchronize()
+        on = o.float().cpu().numpy().reshape(o_ref.shape)
+        assert np.isfinite(on).all(), shape
+        assert np.abs(on - o_ref).max() / den <= TOL_BF16, shape
+    say("band sweep", ci, BAND_CASES[ci], "staged")
+    o, sg = ol.banded_bmm(qg, kg, vg, w, dil, scale, mask_invalid=mask, staged=True,
+                          return_s=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(sg.cpu().numpy().reshape(s_ref.shape), s_ref)
+    on = o.float().cpu().numpy().reshape(o_ref.shape)
+    assert np.abs(on - o_ref).max() / den <= TOL_BF16
